@@ -1,0 +1,172 @@
+"""Benchmark of the progressive approximate-LSTM hot path on one MI355X.
+
+A step is one call of approx_lstm_run over one synthetic driving-shaped
+sequence (D=2048 ReLU-like features, H=512, T=16, batch 1; gate matrices
+2048x2560 per gate factorised to rank 512 with 75% magnitude pruning) at the
+full refinement budget K=512 per gate.  The factorisation (prepare) is setup
+and is not timed.  Inputs are resident in HBM before the timed region.
+
+Prints one JSON line: timesteps/s at K=512, microseconds per timestep, a
+sweep over K = 1..512, the roofline of the run kernel, and the float64 CPU
+oracle timed on a bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes_per_timestep(G, Rg, NZ, C, K, D, H, B, L):
+    """Bytes the method must move per timestep (Eq. (1) streamed once per
+    timestep, as the paper's design streams u and v for every refinement):
+    per term 4*R_g (u) + 6*NZ (fp32 value + 16-bit index; 4*C if v is dense)
+    + 4 (sigma), plus x_t and the h outputs."""
+    v_bytes = 4 * C if NZ == C else 6 * NZ
+    return G * K * (4 * Rg + v_bytes + 4) + 4 * D * B + 4 * H * B * L
+
+
+def algorithmic_flops_per_timestep(G, Rg, NZ, K, B):
+    """N_steps * (2R + 2NZ + 1) per gate (Sec. III), per sequence."""
+    return G * K * (2 * Rg + 2 * NZ + 1) * B
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--prune", type=float, default=0.75)
+    ap.add_argument("--K", type=int, default=512)
+    ap.add_argument("--blocks", type=int, default=0, help="workgroups of the run kernel (0 = automatic)")
+    ap.add_argument("--sweep", default="1,2,4,8,16,32,64,128,256,512")
+    ap.add_argument("--sweep-steps", type=int, default=50)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build has no multi-GPU path; "
+              "independent sequences or levels would shard across GPUs with no exchange.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1905_00689_amd import synth
+    from paper_1905_00689_amd import binding as B
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda")
+    wl = synth.named("driving")
+    D, H, T, Bn = wl.D, wl.H, wl.T, wl.B
+    C = D + H
+    rank = 512
+    t0 = time.time()
+    m = B.approx_lstm_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H, rank, prune_ratio=args.prune, groups=4)
+    prep_s = time.time() - t0
+    info = m.info
+    NZ, G, Rg = info["nz"], info["groups"], info["rows_per_group"]
+    if args.blocks:
+        B.approx_lstm_set_launch(m, args.blocks)
+    B.approx_lstm_reserve(m, T, Bn, 1)
+    x = torch.from_numpy(wl.x).to(dev)
+    h_out = torch.empty((1, T, Bn, H), device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(K, steps, warmup):
+        for _ in range(warmup):
+            B.approx_lstm_run(m, x, [K], h_out, stream=stream)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            B.approx_lstm_run(m, x, [K], h_out, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        B.approx_lstm_check(m)
+        return e0.elapsed_time(e1) / steps   # ms per run
+
+    K = args.K
+    ms = timed(K, args.steps, args.warmup)
+    us_per_ts = ms * 1e3 / T
+    value = T * Bn / (ms * 1e-3)
+
+    sweep = {"K": [], "us_per_timestep": [], "timesteps_per_s": [], "hbm_frac": []}
+    for k in [int(s) for s in args.sweep.split(",") if s]:
+        if k > rank:
+            continue
+        msk = timed(k, args.sweep_steps, 5)
+        byts = T * algorithmic_bytes_per_timestep(G, Rg, NZ, C, k, D, H, Bn, 1)
+        sweep["K"].append(k)
+        sweep["us_per_timestep"].append(round(msk * 1e3 / T, 4))
+        sweep["timesteps_per_s"].append(round(T * Bn / (msk * 1e-3), 1))
+        sweep["hbm_frac"].append(round(byts / (msk * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+
+    bytes_launch = T * algorithmic_bytes_per_timestep(G, Rg, NZ, C, K, D, H, Bn, 1)
+    achieved = bytes_launch / (ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "progressive_lstm_kernel", "bytes_per_launch": bytes_launch,
+                "flops_per_launch": T * algorithmic_flops_per_timestep(G, Rg, NZ, K, Bn)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(m, wl, K, args.cpu_seconds)
+
+    out = {
+        "metric": "LSTM timesteps/sec at refinement budget K (and us/timestep vs K)",
+        "value": round(value, 1), "unit": "timesteps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "driving-shaped LSTM D=2048 H=512 T=16 B=1, per-gate rank 512, "
+                               f"{int(args.prune * 100)}% pruning (NZ={NZ}), K={K}",
+                   "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
+        "us_per_timestep": round(us_per_ts, 4), "prepare_s": round(prep_s, 2),
+        "sweep": sweep, "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(m, wl, K, seconds):
+    """Time the float64 oracle's progressive run on the same workload: the
+    whole T=16 sequence at budget K, repeated for about `seconds`.  The
+    oracle runs on the library's exported terms (timing only: values do not
+    change its cost)."""
+    import oracle
+    from oracle.factorise import Factors
+    from paper_1905_00689_amd import binding as B
+    inf = m.info
+    G, N, Rg, nz, C = inf["groups"], inf["rank"], inf["rows_per_group"], inf["nz"], inf["aug_size"]
+    sig = np.zeros((G, N)); U = np.zeros((G, N, Rg)); mask = np.zeros((G, N, nz), np.int64)
+    vals = np.zeros((G, N, nz))
+    for g in range(G):
+        f = B.approx_lstm_get_factors(m, g)
+        sig[g], U[g], mask[g], vals[g] = f["sigma"], f["u"], f["v_idx"], f["v_val"]
+    fac = Factors(inf["input_size"], inf["hidden_size"], G, N, nz, sig, U, mask, vals,
+                  np.zeros((G, N, 1)), np.array(inf["eff_rank"]), "f32")
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    runs, t0 = 0, time.time()
+    while True:
+        oracle.run(fac, wl.b, wl.x, [K])
+        runs += 1
+        el = time.time() - t0
+        if el >= seconds or runs >= 10000:
+            break
+    ts = runs * wl.T * wl.B
+    return {"value": round(ts / el, 2), "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"oracle.run (float64 NumPy) over the full T={wl.T} sequence at K={K}, "
+                      f"repeated {runs} times ({el:.1f} s), on the library's exported terms"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * approx_lstm.h -- C ABI of the MI355X (gfx950) progressive approximate-LSTM
+ * library.
+ *
+ * Method: "Approximate LSTMs for Time-Constrained Inference" (Rizakis et al.,
+ * arXiv 1905.00689).  Each LSTM gate's augmented matrix W = [W_x W_h]
+ * (Sec. III, "information-maximising approximation") is replaced by an ordered
+ * list of refinement terms sigma^(n) u^(n) prune(v^(n), NZ)^T, each the top
+ * singular triplet of the residual left by the terms before it, with v pruned
+ * to its NZ largest-magnitude entries (Sec. III, Eq. (1) and the residual
+ * definition after it).  Running with a budget of K terms per gate gives a
+ * usable approximation whose quality grows with K; the gate outputs then pass
+ * through the usual sigmoid/tanh cell update (Sec. II, Fig. 1).
+ *
+ * Conventions shared by every call:
+ *   - Every call returns approx_lstm_status; 0 means success.  On error the
+ *     outputs are left untouched and approx_lstm_last_error() (thread-local)
+ *     describes the failure.  No C++ exception crosses this boundary.
+ *   - Host pointers are marked "host", device pointers "device".  The caller
+ *     owns every pointer it passes; the library never frees them and keeps no
+ *     reference after the call returns.
+ *   - Arrays are dense, row-major, float32 unless stated otherwise.
+ *   - Gate rows are stacked in the order i, f, g (cell candidate), o, each
+ *     block H rows tall, as in torch.nn.LSTM.  A bias b = b_ih + b_hh is added
+ *     to the gate pre-activations exactly (outside the approximation).
+ *   - hip_stream is a hipStream_t (NULL = the default stream).  Device work is
+ *     enqueued on it asynchronously unless stated otherwise.
+ *   - A model is immutable after approx_lstm_prepare except for its run
+ *     workspace; calls that use one model on several streams at once race on
+ *     that workspace and must be serialised by the caller.
+ */
+#ifndef APPROX_LSTM_H
+#define APPROX_LSTM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  APPROX_LSTM_OK = 0,
+  APPROX_LSTM_ERR_INVALID_ARG = 1,         /* null pointer, size <= 0, nz not in [1,C], rank < 1,
+                                              a level K outside [0,rank], groups not 1 or 4 */
+  APPROX_LSTM_ERR_OUT_OF_MEMORY = 2,       /* host or device allocation failed */
+  APPROX_LSTM_ERR_DEVICE = 3,              /* HIP runtime failure or a device-side wait that
+                                              exceeded its spin limit */
+  APPROX_LSTM_ERR_NOT_CONVERGED = 4,       /* prepare: a top-triplet solve missed its tolerance;
+                                              the model is still returned, with the count in info */
+  APPROX_LSTM_ERR_DEADLINE_INFEASIBLE = 5, /* even K = 0 misses the requested deadline */
+  APPROX_LSTM_ERR_UNSUPPORTED = 6          /* a size or combination this build does not handle
+                                              (e.g. C > 65535, more levels than APPROX_LSTM_MAX_LEVELS) */
+} approx_lstm_status;
+
+#define APPROX_LSTM_MAX_LEVELS 16
+
+/* prepare flags */
+#define APPROX_LSTM_FLAG_HOST_ONLY      (1ull << 0) /* factorise on the host only; no device store
+                                                       (get_factors works, run returns INVALID_ARG) */
+#define APPROX_LSTM_FLAG_KEEP_UNPRUNED  (1ull << 1) /* keep the fp64 sigma, u and unpruned v of every
+                                                       term for approx_lstm_get_factors_f64 */
+
+typedef struct approx_lstm_model approx_lstm_model;   /* opaque */
+
+typedef struct {
+  int32_t input_size;   /* D >= 1 */
+  int32_t hidden_size;  /* H >= 1; C = D + H must be <= 65535 */
+  int32_t rank;         /* N >= 1: refinement terms stored per group (the paper's maximum N_steps) */
+  int32_t nz;           /* NZ kept per v, 1..C; 0 means nz = C - floor(prune_ratio * C) with the
+                           product taken as one IEEE double multiplication */
+  double prune_ratio;   /* p in [0, 1); used only when nz == 0 */
+  int32_t groups;       /* 4: each gate's H x C block is factorised separately (the paper's scheme);
+                           1: the stacked 4H x C matrix is factorised as one */
+  int32_t factor_dtype; /* 0 = fp32 factors (the only value this build accepts) */
+  uint64_t flags;       /* APPROX_LSTM_FLAG_* */
+} approx_lstm_prepare_params;
+
+typedef struct {
+  int32_t input_size, hidden_size, aug_size;  /* D, H, C */
+  int32_t groups, rows_per_group;             /* G, R_g = 4H / G */
+  int32_t rank, nz;                           /* N, NZ */
+  int32_t eff_rank[4];                        /* live terms per group (later terms are zero) */
+  int32_t unconverged_steps;                  /* solves that missed tolerance (0 normally) */
+  int32_t has_device_store;
+  uint64_t device_bytes;                      /* factor store on the device */
+} approx_lstm_info;
+
+/*
+ * approx_lstm_prepare -- factorise and prune the gate weights (Sec. III,
+ * Eq. (1)); upload the packed factor store to the current device.
+ *
+ *   w_ih  host [4H][D]   input weights   (W_x of every gate)
+ *   w_hh  host [4H][H]   recurrent weights (W_h of every gate)
+ *   bias  host [4H] or NULL (zeros)
+ *   p     host, see approx_lstm_prepare_params
+ *   out   host; receives the new model (destroy with approx_lstm_destroy)
+ *
+ * Per group, in float64 on the host: R <- W_g; for n = 1..rank: the top
+ * singular triplet (sigma, u, v) of R (Lanczos on R R^T or R^T R with full
+ * reorthogonalisation, then sigma and the other vector from one product with
+ * R); sign fixed so that v's largest-magnitude entry (lowest index on ties) is
+ * positive; mask = the NZ entries of largest |v| (ties to the lower index),
+ * ascending; R <- R - sigma u prune(v)^T.  A step with sigma <= 1e-12 times
+ * the first step's sigma ends the list: that and every later term are zero.
+ * Values are then rounded to fp32 (nearest even).  Synchronises hip_stream
+ * before returning.  Returns NOT_CONVERGED (with a usable model) if a solve
+ * missed its tolerance.
+ */
+approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, const float* bias,
+                                       const approx_lstm_prepare_params* p, void* hip_stream,
+                                       approx_lstm_model** out);
+
+/*
+ * approx_lstm_run -- progressive LSTM over a sequence at one or more
+ * refinement budgets (Eq. (1) per gate, then the Sec. II cell update).
+ *
+ *   x        device [T][B][D]
+ *   T, B     sequence length (T >= 0; T == 0 does nothing) and batch (B >= 1)
+ *   h0, c0   device [B][H] or NULL (zeros)
+ *   levels   host [n_levels]; each K in [0, rank] is the number of refinement
+ *            terms used per group at every timestep
+ *   n_levels 1..APPROX_LSTM_MAX_LEVELS
+ *   h_out    device [n_levels][T][B][H]: h_t of each level
+ *   c_out    device [n_levels][B][H] or NULL: final cell state of each level
+ *
+ * Each level is its own recurrence (its h feeds only itself); the x-part of
+ * the projections is shared.  Asynchronous on hip_stream; the call blocks
+ * only to allocate workspace on first use (see approx_lstm_reserve).  The
+ * device-side waits of the kernel are bounded; if one expires the next
+ * approx_lstm_check call reports APPROX_LSTM_ERR_DEVICE.
+ */
+approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                   const float* h0, const float* c0, const int32_t* levels,
+                                   int32_t n_levels, float* h_out, float* c_out, void* hip_stream);
+
+/*
+ * approx_lstm_reserve -- preallocate the run workspace for up to T_max
+ * timesteps, B_max sequences and L_max levels, so that later runs within
+ * those sizes allocate nothing.  Blocking.
+ */
+approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int32_t B_max,
+                                       int32_t L_max);
+
+/*
+ * approx_lstm_check -- synchronise hip_stream and report whether any device
+ * wait of an earlier run on this model expired (APPROX_LSTM_ERR_DEVICE) or a
+ * HIP error is pending.  Clears the recorded flag.
+ */
+approx_lstm_status approx_lstm_check(approx_lstm_model* m, void* hip_stream);
+
+/*
+ * approx_lstm_set_launch -- number of workgroups the run kernel uses
+ * (0 = automatic: about one per 16 terms in use, at most 128 and at most the
+ * device's compute units).  Takes effect on the next run; a tuning knob, the
+ * results do not depend on it beyond float32 summation order.
+ */
+approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks);
+
+/* approx_lstm_model_info -- sizes, live ranks and device footprint (host struct). */
+approx_lstm_status approx_lstm_model_info(const approx_lstm_model* m, approx_lstm_info* out);
+
+/*
+ * approx_lstm_get_factors -- copy group g's refinement terms, in refinement
+ * order, as the device store holds them (fp32), to host arrays:
+ *   sigma [rank], u [rank][R_g], v_idx [rank][nz] (ascending column indices
+ *   into [x; h], 0..C-1), v_val [rank][nz] (entries of prune(v) on v_idx).
+ * Any output pointer may be NULL.  Reads the host copy kept by prepare.
+ */
+approx_lstm_status approx_lstm_get_factors(const approx_lstm_model* m, int32_t group, float* sigma,
+                                           float* u, int32_t* v_idx, float* v_val);
+
+/*
+ * approx_lstm_get_factors_f64 -- the float64 sigma [rank], u [rank][R_g] and
+ * unpruned v [rank][C] of group g before rounding (for certificates).  Needs
+ * APPROX_LSTM_FLAG_KEEP_UNPRUNED at prepare time, else INVALID_ARG.
+ */
+approx_lstm_status approx_lstm_get_factors_f64(const approx_lstm_model* m, int32_t group,
+                                               double* sigma, double* u, double* v_unpruned);
+
+/* approx_lstm_destroy -- free the model and its device memory (NULL is a no-op). */
+void approx_lstm_destroy(approx_lstm_model* m);
+
+/* approx_lstm_last_error -- text of the last error on this thread ("" if none). */
+const char* approx_lstm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* APPROX_LSTM_H */

@@ -1,0 +1,455 @@
+// C-ABI implementation: argument checking, host factorisation (float64),
+// packing of the device factor store, run workspace and kernel launch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/approx_lstm.h"
+#include "factorise.hpp"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+approx_lstm_status fail(approx_lstm_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+approx_lstm_status hip_fail(hipError_t e, const char* what) {
+  if (e == hipErrorOutOfMemory)
+    return fail(APPROX_LSTM_ERR_OUT_OF_MEMORY, "%s: %s", what, hipGetErrorString(e));
+  return fail(APPROX_LSTM_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                    \
+  do {                                         \
+    hipError_t _e = (expr);                    \
+    if (_e != hipSuccess) return hip_fail(_e, what); \
+  } while (0)
+
+template <class T>
+void dfree(T*& p) {
+  if (p) (void)hipFree((void*)p);
+  p = nullptr;
+}
+
+// Sets the model's device current for the scope and restores the caller's.
+struct DeviceScope {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceScope(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceScope() {
+    int cur;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+}  // namespace
+
+struct approx_lstm_model {
+  int D = 0, H = 0, C = 0, G = 0, Rg = 0, N = 0, NZ = 0;
+  uint64_t flags = 0;
+  int eff_rank[4] = {0, 0, 0, 0};
+  int unconverged = 0;
+  // host copies, as stored (fp32) -- [G][N]..., per group
+  std::vector<float> sigma, u, vval, bias;
+  std::vector<int32_t> vidx;
+  std::vector<double> sigma64, u64, v64;   // only with KEEP_UNPRUNED
+  // device factor store
+  int device = -1;
+  bool has_dev = false;
+  float* d_sigma = nullptr;
+  float* d_Ut = nullptr;
+  float* d_vval = nullptr;
+  float* d_bias = nullptr;
+  uint16_t* d_vidx = nullptr;
+  uint16_t* d_nx = nullptr;
+  uint64_t dev_bytes = 0;
+  int num_cu = 0;
+  // run workspace
+  float* d_px = nullptr;
+  size_t px_cap = 0;                 // floats
+  unsigned long long* d_zx = nullptr;
+  size_t zx_cap = 0;                 // words
+  unsigned long long* d_hx = nullptr;
+  size_t hx_cap = 0;
+  unsigned* d_err = nullptr;
+  unsigned seq = 0;
+  int launch_blocks = 0;             // 0 = automatic
+
+  ~approx_lstm_model() {
+    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err) return;
+    DeviceScope ds(device);
+    dfree(d_sigma);
+    dfree(d_Ut);
+    dfree(d_vval);
+    dfree(d_bias);
+    dfree(d_vidx);
+    dfree(d_nx);
+    dfree(d_px);
+    dfree(d_zx);
+    dfree(d_hx);
+    dfree(d_err);
+  }
+};
+
+namespace {
+
+approx_lstm_status ensure_workspace(approx_lstm_model* m, size_t px_floats, size_t zx_words, size_t hx_words,
+                                    hipStream_t stream) {
+  bool fresh = false;
+  if (!m->d_err) {
+    HIP_TRY(hipMalloc(&m->d_err, 64), "hipMalloc(err)");
+    HIP_TRY(hipMemsetAsync(m->d_err, 0, 64, stream), "hipMemsetAsync(err)");
+  }
+  if (px_floats > m->px_cap) {
+    HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    dfree(m->d_px);
+    m->px_cap = 0;
+    HIP_TRY(hipMalloc(&m->d_px, px_floats * sizeof(float)), "hipMalloc(px)");
+    m->px_cap = px_floats;
+  }
+  if (zx_words > m->zx_cap) {
+    HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    dfree(m->d_zx);
+    m->zx_cap = 0;
+    HIP_TRY(hipMalloc(&m->d_zx, zx_words * 8), "hipMalloc(zx)");
+    m->zx_cap = zx_words;
+    fresh = true;
+  }
+  if (hx_words > m->hx_cap) {
+    HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    dfree(m->d_hx);
+    m->hx_cap = 0;
+    HIP_TRY(hipMalloc(&m->d_hx, hx_words * 8), "hipMalloc(hx)");
+    m->hx_cap = hx_words;
+    fresh = true;
+  }
+  if (fresh) {
+    // New exchange memory: clear every tag before its first use.
+    if (m->d_zx) HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
+    if (m->d_hx) HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+    m->seq = 0;
+  }
+  return APPROX_LSTM_OK;
+}
+
+int auto_blocks(const approx_lstm_model* m, int GK) {
+  int cap = std::max(1, std::min(m->num_cu, 128));
+  int want = (GK + 15) / 16;
+  return std::max(1, std::min(cap, want));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* approx_lstm_last_error(void) { return g_last_error.c_str(); }
+
+approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, const float* bias,
+                                       const approx_lstm_prepare_params* p, void* hip_stream,
+                                       approx_lstm_model** out) {
+  g_last_error.clear();
+  if (!w_ih || !w_hh || !p || !out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null pointer argument");
+  const int D = p->input_size, H = p->hidden_size;
+  if (D < 1 || H < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "input_size and hidden_size must be >= 1");
+  const long long Cll = (long long)D + H;
+  if (Cll > 65535) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "D + H = %lld exceeds 65535", Cll);
+  const int C = (int)Cll;
+  if (p->groups != 1 && p->groups != 4) return fail(APPROX_LSTM_ERR_INVALID_ARG, "groups must be 1 or 4");
+  if (p->rank < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "rank must be >= 1");
+  if (p->factor_dtype != 0) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "only fp32 factors (factor_dtype 0) are built");
+  int nz = p->nz;
+  if (nz == 0) {
+    if (!(p->prune_ratio >= 0.0 && p->prune_ratio < 1.0))
+      return fail(APPROX_LSTM_ERR_INVALID_ARG, "prune_ratio must be in [0, 1)");
+    nz = C - (int)std::floor(p->prune_ratio * (double)C);
+  }
+  if (nz < 1 || nz > C) return fail(APPROX_LSTM_ERR_INVALID_ARG, "nz = %d not in [1, %d]", nz, C);
+  const bool host_only = (p->flags & APPROX_LSTM_FLAG_HOST_ONLY) != 0;
+  const bool keep = (p->flags & APPROX_LSTM_FLAG_KEEP_UNPRUNED) != 0;
+
+  approx_lstm_model* m = new (std::nothrow) approx_lstm_model();
+  if (!m) return fail(APPROX_LSTM_ERR_OUT_OF_MEMORY, "host allocation failed");
+  const int G = p->groups, Rg = 4 * H / G, N = p->rank;
+  m->D = D; m->H = H; m->C = C; m->G = G; m->Rg = Rg; m->N = N; m->NZ = nz; m->flags = p->flags;
+
+  std::vector<alstm::GroupFactors> gf(G);
+  try {
+    std::vector<double> W((size_t)4 * H * C);
+    for (int o = 0; o < 4 * H; ++o) {
+      for (int k = 0; k < D; ++k) W[(size_t)o * C + k] = w_ih[(size_t)o * D + k];
+      for (int k = 0; k < H; ++k) W[(size_t)o * C + D + k] = w_hh[(size_t)o * H + k];
+    }
+    alstm::FactoriseOptions opt;
+    opt.keep_unpruned = keep;
+    std::vector<std::thread> th;
+    for (int g = 0; g < G; ++g)
+      th.emplace_back([&, g] { alstm::factorise_group(&W[(size_t)g * Rg * C], Rg, C, N, nz, opt, gf[g]); });
+    for (auto& t : th) t.join();
+
+    m->sigma.assign((size_t)G * N, 0.f);
+    m->u.assign((size_t)G * N * Rg, 0.f);
+    m->vidx.assign((size_t)G * N * nz, 0);
+    m->vval.assign((size_t)G * N * nz, 0.f);
+    m->bias.assign((size_t)4 * H, 0.f);
+    if (bias) std::copy(bias, bias + 4 * H, m->bias.begin());
+    if (keep) {
+      m->sigma64.assign((size_t)G * N, 0.0);
+      m->u64.assign((size_t)G * N * Rg, 0.0);
+      m->v64.assign((size_t)G * N * C, 0.0);
+    }
+    for (int g = 0; g < G; ++g) {
+      m->eff_rank[g] = gf[g].eff_rank;
+      m->unconverged += gf[g].unconverged;
+      for (int n = 0; n < N; ++n) {
+        m->sigma[(size_t)g * N + n] = (float)gf[g].sigma[n];
+        for (int r = 0; r < Rg; ++r) m->u[((size_t)g * N + n) * Rg + r] = (float)gf[g].u[(size_t)n * Rg + r];
+        for (int e = 0; e < nz; ++e) {
+          m->vidx[((size_t)g * N + n) * nz + e] = gf[g].mask[(size_t)n * nz + e];
+          m->vval[((size_t)g * N + n) * nz + e] = (float)gf[g].vals[(size_t)n * nz + e];
+        }
+      }
+      if (keep) {
+        std::copy(gf[g].sigma.begin(), gf[g].sigma.end(), m->sigma64.begin() + (size_t)g * N);
+        std::copy(gf[g].u.begin(), gf[g].u.end(), m->u64.begin() + (size_t)g * N * Rg);
+        std::copy(gf[g].v.begin(), gf[g].v.end(), m->v64.begin() + (size_t)g * N * C);
+      }
+    }
+  } catch (const std::bad_alloc&) {
+    delete m;
+    return fail(APPROX_LSTM_ERR_OUT_OF_MEMORY, "host allocation failed during factorisation");
+  } catch (const std::exception& ex) {
+    delete m;
+    return fail(APPROX_LSTM_ERR_DEVICE, "factorisation failed: %s", ex.what());
+  }
+
+  if (!host_only) {
+    // Pack the device store: term tau = n*G + g in refinement order.
+    const size_t NT = (size_t)N * G;
+    std::vector<float> s_h(NT), Ut_h((size_t)4 * H * N), vv_h(NT * nz);
+    std::vector<uint16_t> vi_h(NT * nz), nx_h(NT);
+    for (int n = 0; n < N; ++n)
+      for (int g = 0; g < G; ++g) {
+        const size_t tau = (size_t)n * G + g, src = (size_t)g * N + n;
+        s_h[tau] = m->sigma[src];
+        int cnt = 0;
+        for (int e = 0; e < nz; ++e) {
+          const int32_t k = m->vidx[src * nz + e];
+          vi_h[tau * nz + e] = (uint16_t)k;
+          vv_h[tau * nz + e] = m->vval[src * nz + e];
+          cnt += (k < D) ? 1 : 0;
+        }
+        nx_h[tau] = (uint16_t)cnt;
+      }
+    for (int o = 0; o < 4 * H; ++o) {
+      const int g = o / Rg, r = o % Rg;
+      for (int n = 0; n < N; ++n) Ut_h[(size_t)o * N + n] = m->u[((size_t)g * N + n) * Rg + r];
+    }
+    approx_lstm_status st = APPROX_LSTM_OK;
+    auto step = [&](hipError_t e, const char* what) {
+      if (st == APPROX_LSTM_OK && e != hipSuccess) st = hip_fail(e, what);
+    };
+    hipStream_t stream = (hipStream_t)hip_stream;
+    step(hipGetDevice(&m->device), "hipGetDevice");
+    if (st == APPROX_LSTM_OK) {
+      hipDeviceProp_t prop;
+      step(hipGetDeviceProperties(&prop, m->device), "hipGetDeviceProperties");
+      m->num_cu = prop.multiProcessorCount;
+    }
+    m->has_dev = true;
+    step(hipMalloc(&m->d_sigma, NT * 4), "hipMalloc(sigma)");
+    step(hipMalloc(&m->d_Ut, Ut_h.size() * 4), "hipMalloc(Ut)");
+    step(hipMalloc(&m->d_vval, vv_h.size() * 4), "hipMalloc(vval)");
+    step(hipMalloc(&m->d_vidx, vi_h.size() * 2), "hipMalloc(vidx)");
+    step(hipMalloc(&m->d_nx, NT * 2), "hipMalloc(nx)");
+    step(hipMalloc(&m->d_bias, (size_t)4 * H * 4), "hipMalloc(bias)");
+    if (st == APPROX_LSTM_OK) {
+      step(hipMemcpyAsync(m->d_sigma, s_h.data(), NT * 4, hipMemcpyHostToDevice, stream), "upload sigma");
+      step(hipMemcpyAsync(m->d_Ut, Ut_h.data(), Ut_h.size() * 4, hipMemcpyHostToDevice, stream), "upload Ut");
+      step(hipMemcpyAsync(m->d_vval, vv_h.data(), vv_h.size() * 4, hipMemcpyHostToDevice, stream), "upload vval");
+      step(hipMemcpyAsync(m->d_vidx, vi_h.data(), vi_h.size() * 2, hipMemcpyHostToDevice, stream), "upload vidx");
+      step(hipMemcpyAsync(m->d_nx, nx_h.data(), NT * 2, hipMemcpyHostToDevice, stream), "upload nx");
+      step(hipMemcpyAsync(m->d_bias, m->bias.data(), (size_t)4 * H * 4, hipMemcpyHostToDevice, stream),
+           "upload bias");
+      step(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    }
+    if (st != APPROX_LSTM_OK) {
+      delete m;
+      return st;
+    }
+    m->dev_bytes = NT * 4 + Ut_h.size() * 4 + vv_h.size() * 4 + vi_h.size() * 2 + NT * 2 + (size_t)4 * H * 4;
+  }
+  *out = m;
+  if (m->unconverged)
+    return fail(APPROX_LSTM_ERR_NOT_CONVERGED, "%d top-triplet solves missed tolerance", m->unconverged);
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int32_t B_max, int32_t L_max) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (!m->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "model has no device store (HOST_ONLY)");
+  if (T_max < 1 || B_max < 1 || L_max < 1 || L_max > APPROX_LSTM_MAX_LEVELS)
+    return fail(APPROX_LSTM_ERR_INVALID_ARG, "reserve sizes out of range");
+  DeviceScope ds(m->device);
+  if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  const size_t GK = (size_t)m->G * m->N, LB = (size_t)L_max * B_max;
+  approx_lstm_status st = ensure_workspace(m, GK * T_max * B_max, LB * GK, LB * m->H, nullptr);
+  if (st != APPROX_LSTM_OK) return st;
+  HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                   const float* h0, const float* c0, const int32_t* levels,
+                                   int32_t n_levels, float* h_out, float* c_out, void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (!m->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "model has no device store (HOST_ONLY)");
+  if (T < 0 || B < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need T >= 0 and B >= 1");
+  if (T > 65534) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T = %d exceeds 65534", T);
+  if (!levels || n_levels < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need at least one level");
+  if (n_levels > APPROX_LSTM_MAX_LEVELS)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "at most %d levels per run", APPROX_LSTM_MAX_LEVELS);
+  int kmax = 0;
+  for (int l = 0; l < n_levels; ++l) {
+    if (levels[l] < 0 || levels[l] > m->N)
+      return fail(APPROX_LSTM_ERR_INVALID_ARG, "level %d: K = %d not in [0, %d]", l, levels[l], m->N);
+    kmax = std::max(kmax, (int)levels[l]);
+  }
+  if (T == 0) return APPROX_LSTM_OK;
+  if (!x || !h_out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null x or h_out");
+
+  DeviceScope ds(m->device);
+  if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  hipStream_t stream = (hipStream_t)hip_stream;
+
+  alstm::RunArgs a{};
+  a.D = m->D; a.H = m->H; a.G = m->G; a.N = m->N; a.NZ = m->NZ; a.T = T; a.B = B; a.L = n_levels;
+  a.GK = m->G * kmax;
+  for (int l = 0; l < n_levels; ++l) a.levels[l] = levels[l];
+  const int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, std::max(1, m->num_cu)) : auto_blocks(m, a.GK);
+  a.rows_per = (m->H + P - 1) / P;
+  const size_t LB = (size_t)n_levels * B;
+  const size_t lds_cap = 160 * 1024;
+  // largest (t, b) chunk of x that fits next to the rest of the LDS layout
+  a.xchunk = 1;
+  {
+    alstm::RunArgs probe = a;
+    probe.xchunk = 1;
+    const size_t fixed = alstm::progressive_lds_bytes(probe) - sizeof(float) * std::max<size_t>(m->D, a.GK);
+    const size_t room = lds_cap > fixed ? (lds_cap - fixed) / (sizeof(float) * m->D) : 0;
+    a.xchunk = (int)std::max<size_t>(1, std::min<size_t>({room, (size_t)alstm::kMaxXChunk, (size_t)T * B}));
+  }
+  if (alstm::progressive_lds_bytes(a) > lds_cap)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "LDS need %zu bytes exceeds 160 KiB (H=%d, levels*B=%zu, G*K=%d)",
+                alstm::progressive_lds_bytes(a), m->H, LB, a.GK);
+
+  approx_lstm_status st =
+      ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * a.GK), LB * m->H, stream);
+  if (st != APPROX_LSTM_OK) return st;
+  m->seq = (m->seq + 1) & 0xFFFFu;
+  if (m->seq == 0) {
+    // tag space wrapped: clear the exchange words so no stale tag can match
+    HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
+    HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+    m->seq = 1;
+  }
+  a.tag_base = m->seq << 16;
+  a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
+  a.sigma = m->d_sigma; a.Ut = m->d_Ut; a.vidx = m->d_vidx; a.vval = m->d_vval; a.nx = m->d_nx;
+  a.bias = m->d_bias; a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx; a.err = m->d_err;
+  HIP_TRY(alstm::launch_progressive(a, P, stream), "launch progressive_lstm_kernel");
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_check(approx_lstm_model* m, void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (!m->has_dev) return APPROX_LSTM_OK;
+  DeviceScope ds(m->device);
+  hipStream_t stream = (hipStream_t)hip_stream;
+  HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+  if (!m->d_err) return APPROX_LSTM_OK;
+  unsigned flag = 0;
+  HIP_TRY(hipMemcpy(&flag, m->d_err, sizeof flag, hipMemcpyDeviceToHost), "read error flag");
+  if (flag) {
+    HIP_TRY(hipMemset(m->d_err, 0, sizeof flag), "clear error flag");
+    return fail(APPROX_LSTM_ERR_DEVICE, "a device-side exchange wait exceeded its spin limit");
+  }
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks) {
+  g_last_error.clear();
+  if (!m || blocks < 0) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
+  m->launch_blocks = blocks;
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_model_info(const approx_lstm_model* m, approx_lstm_info* out) {
+  g_last_error.clear();
+  if (!m || !out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null pointer argument");
+  std::memset(out, 0, sizeof *out);
+  out->input_size = m->D;
+  out->hidden_size = m->H;
+  out->aug_size = m->C;
+  out->groups = m->G;
+  out->rows_per_group = m->Rg;
+  out->rank = m->N;
+  out->nz = m->NZ;
+  for (int g = 0; g < 4; ++g) out->eff_rank[g] = g < m->G ? m->eff_rank[g] : 0;
+  out->unconverged_steps = m->unconverged;
+  out->has_device_store = m->has_dev ? 1 : 0;
+  out->device_bytes = m->dev_bytes;
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_get_factors(const approx_lstm_model* m, int32_t group, float* sigma, float* u,
+                                           int32_t* v_idx, float* v_val) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (group < 0 || group >= m->G) return fail(APPROX_LSTM_ERR_INVALID_ARG, "group %d out of range", group);
+  const size_t N = m->N, Rg = m->Rg, nz = m->NZ;
+  if (sigma) std::copy_n(m->sigma.begin() + group * N, N, sigma);
+  if (u) std::copy_n(m->u.begin() + group * N * Rg, N * Rg, u);
+  if (v_idx) std::copy_n(m->vidx.begin() + group * N * nz, N * nz, v_idx);
+  if (v_val) std::copy_n(m->vval.begin() + group * N * nz, N * nz, v_val);
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_get_factors_f64(const approx_lstm_model* m, int32_t group, double* sigma,
+                                               double* u, double* v_unpruned) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (group < 0 || group >= m->G) return fail(APPROX_LSTM_ERR_INVALID_ARG, "group %d out of range", group);
+  if (m->sigma64.empty()) return fail(APPROX_LSTM_ERR_INVALID_ARG, "prepared without KEEP_UNPRUNED");
+  const size_t N = m->N, Rg = m->Rg, C = m->C;
+  if (sigma) std::copy_n(m->sigma64.begin() + group * N, N, sigma);
+  if (u) std::copy_n(m->u64.begin() + group * N * Rg, N * Rg, u);
+  if (v_unpruned) std::copy_n(m->v64.begin() + group * N * C, N * C, v_unpruned);
+  return APPROX_LSTM_OK;
+}
+
+void approx_lstm_destroy(approx_lstm_model* m) { delete m; }
+
+}  // extern "C"

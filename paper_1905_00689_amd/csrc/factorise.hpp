@@ -1,0 +1,43 @@
+// Host-side float64 factorisation of one gate group into pruned rank-1
+// refinement terms (Sec. III, Eq. (1) of arXiv 1905.00689).  Plain C++17,
+// no HIP.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+namespace alstm {
+
+struct GroupFactors {
+  int rows = 0, cols = 0, rank = 0, nz = 0;
+  std::vector<double> sigma;    // [rank]
+  std::vector<double> u;        // [rank][rows]
+  std::vector<double> v;        // [rank][cols] unpruned (only if keep_unpruned)
+  std::vector<int32_t> mask;    // [rank][nz] ascending column indices
+  std::vector<double> vals;     // [rank][nz] entries of v on the mask
+  int eff_rank = 0;             // live terms; terms >= eff_rank are zero
+  int unconverged = 0;          // solves that missed the Lanczos tolerance
+};
+
+struct FactoriseOptions {
+  bool keep_unpruned = false;
+  int gram_refresh = 8;         // recompute the Gram matrix exactly every this many steps
+  double lanczos_tol = 4e-14;   // Ritz residual / Ritz value at which a solve stops
+  double stop_rel = 1e-12;      // sigma <= stop_rel * sigma_1 ends the term list
+  int max_lanczos = 0;          // 0: up to the Gram size
+};
+
+// Factorise W (rows x cols, row-major, float64) into `rank` terms keeping
+// `nz` entries of each v.  Returns 0, or 1 if a solve did not converge (the
+// result is still complete).
+int factorise_group(const double* W, int rows, int cols, int rank, int nz,
+                    const FactoriseOptions& opt, GroupFactors& out);
+
+// Top eigenpair of the symmetric n x n matrix G (row-major) by Lanczos with
+// full reorthogonalisation from a fixed pseudo-random start.  Writes the unit
+// eigenvector to y and returns the eigenvalue; *converged tells whether the
+// Ritz residual met tol (relative to the eigenvalue).
+double lanczos_top(const double* G, int n, double tol, int max_iter, double* y, bool* converged,
+                   int* iterations);
+
+}  // namespace alstm

@@ -1,0 +1,198 @@
+"""Parity of the HIP run path (through the C ABI) with the float64 oracle.
+
+Error measure: for every (level, timestep, sequence), the max-abs difference
+of the H-vector h divided by max(||h_oracle||_inf, 1e-6); the bar is 1e-4
+for the fp32 path.  Where the oracle's factor chain is independent of the
+library's (tiny workload, and the first steps of the driving workload), the
+oracle prepares its own factors; past the chain's agreement horizon (the
+residual-SVD-with-pruning chain is numerically chaotic, see
+test_library_cpu.py) the oracle runs on the library's exported terms, which
+test_library_cpu.py certifies step by step against the oracle.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.factorise import Factors
+from paper_1905_00689_amd import synth
+from paper_1905_00689_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def rel_err(h_gpu, h_orc):
+    num = np.abs(h_gpu - h_orc).max(axis=-1)
+    den = np.maximum(np.abs(h_orc).max(axis=-1), 1e-6)
+    return float((num / den).max())
+
+
+def prep(w, rank, p, groups=4, flags=0):
+    D, H = w.D, w.H
+    return B.approx_lstm_prepare(w.W[:, :D], w.W[:, D:], w.b, D, H, rank, prune_ratio=p,
+                                 groups=groups, flags=flags)
+
+
+def run_gpu(m, x, levels, h0=None, c0=None, want_c=False):
+    T, Bn, D = x.shape
+    H = m.info["hidden_size"]
+    dev = torch.device("cuda")
+    xt = torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(dev)
+    h_out = torch.full((len(levels), T, Bn, H), float("nan"), device=dev)
+    c_out = torch.full((len(levels), Bn, H), float("nan"), device=dev) if want_c else None
+    h0t = None if h0 is None else torch.from_numpy(np.ascontiguousarray(h0, np.float32)).to(dev)
+    c0t = None if c0 is None else torch.from_numpy(np.ascontiguousarray(c0, np.float32)).to(dev)
+    B.approx_lstm_run(m, xt, levels, h_out, h0t, c0t, c_out)
+    B.approx_lstm_check(m)
+    torch.cuda.synchronize()
+    return h_out.cpu().numpy(), (c_out.cpu().numpy() if want_c else None)
+
+
+def exported_factors(m):
+    """The library's stored terms as an oracle Factors object (fp32 values)."""
+    inf = m.info
+    G, N, Rg, nz, C = inf["groups"], inf["rank"], inf["rows_per_group"], inf["nz"], inf["aug_size"]
+    sig = np.zeros((G, N)); U = np.zeros((G, N, Rg)); mask = np.zeros((G, N, nz), np.int64)
+    vals = np.zeros((G, N, nz))
+    for g in range(G):
+        f = B.approx_lstm_get_factors(m, g)
+        sig[g], U[g], mask[g], vals[g] = f["sigma"], f["u"], f["v_idx"], f["v_val"]
+    return Factors(inf["input_size"], inf["hidden_size"], G, N, nz, sig, U, mask, vals,
+                   np.zeros((G, N, C)), np.array(inf["eff_rank"]), "f32")
+
+
+# ------------------------------------------------------------------ tiny
+@pytest.mark.parametrize("G", [4, 1])
+@pytest.mark.parametrize("p", [0.0, 0.5])
+def test_tiny_every_level_matches_oracle(G, p):
+    w = synth.named("tiny")
+    levels = [0, 1, 4, 16, 96]
+    say("tiny", "G", G, "p", p, "levels", levels)
+    m = prep(w, 96, p, G)
+    f = oracle.prepare(w.W, 32, 96, oracle.nz_from_ratio(96, p), groups=G)
+    h, _ = run_gpu(m, w.x, levels)
+    ho, _ = oracle.run(f, w.b, w.x, levels)
+    for j, K in enumerate(levels):
+        assert rel_err(h[j], ho[j]) < TOL, (K, rel_err(h[j], ho[j]))
+    if p == 0.0:
+        he, _ = oracle.exact_lstm(w.W, w.b, w.x)
+        assert rel_err(h[-1], he) < TOL          # full rank, no pruning: the exact LSTM
+
+
+def test_tiny_batch_with_initial_state_and_final_cell():
+    w = synth.make(64, 32, 6, 3, index=11, xkind="normal")
+    rng = np.random.default_rng(5)
+    h0 = rng.normal(size=(3, 32)).astype(np.float32)
+    c0 = rng.normal(size=(3, 32)).astype(np.float32)
+    levels = [0, 7, 96]
+    say("tiny batch 3 with h0/c0", levels)
+    m = prep(w, 96, 0.5)
+    f = oracle.prepare(w.W, 32, 96, 48)
+    h, c = run_gpu(m, w.x, levels, h0, c0, want_c=True)
+    ho, co = oracle.run(f, w.b, w.x, levels, h0, c0)
+    assert rel_err(h, ho) < TOL
+    assert np.abs(c - co).max() < 1e-4 * max(1.0, np.abs(co).max())
+
+
+@pytest.mark.parametrize("G", [4, 1])
+def test_ragged_shapes_and_launch_widths(G):
+    """D, H not multiples of anything; hidden units split unevenly over the
+    workgroups; K = 0, partial and full; results must not depend on the
+    number of workgroups (every sum has a fixed order)."""
+    w = synth.make(50, 37, 5, 2, index=12, xkind="relu")
+    rank = 20
+    levels = [0, 3, rank]
+    say("ragged D=50 H=37 G", G)
+    m = prep(w, rank, 0.6, G)
+    f = oracle.prepare(w.W, 37, rank, oracle.nz_from_ratio(87, 0.6), groups=G)
+    ref = None
+    for P in (0, 1, 5, 16, 37, 64):
+        say("  blocks", P)
+        B.approx_lstm_set_launch(m, P)
+        h, _ = run_gpu(m, w.x, levels)
+        ho, _ = oracle.run(f, w.b, w.x, levels)
+        assert rel_err(h, ho) < TOL, P
+        if ref is None:
+            ref = h
+        else:
+            assert np.array_equal(h, ref), P
+
+
+def test_zero_length_sequence_and_bad_levels():
+    w = synth.named("tiny")
+    m = prep(w, 8, 0.5)
+    say("T=0 and argument errors")
+    x = torch.zeros((0, 1, 64), device="cuda")
+    h = torch.zeros((1, 0, 1, 32), device="cuda")
+    assert B.approx_lstm_run(m, x, [4], h) == B.OK
+    xt = torch.zeros((2, 1, 64), device="cuda")
+    ht = torch.zeros((1, 2, 1, 32), device="cuda")
+    with pytest.raises(B.ApproxLstmError) as ei:
+        B.approx_lstm_run(m, xt, [9], ht)
+    assert ei.value.status == B.ERR_INVALID_ARG
+    with pytest.raises(B.ApproxLstmError) as ei:
+        B.approx_lstm_run(m, xt, [-1], ht)
+    assert ei.value.status == B.ERR_INVALID_ARG
+    h17 = torch.zeros((17, 2, 1, 32), device="cuda")
+    with pytest.raises(B.ApproxLstmError) as ei:
+        B.approx_lstm_run(m, xt, [1] * 17, h17)
+    assert ei.value.status == B.ERR_UNSUPPORTED
+
+
+# --------------------------------------------------------------- driving
+@pytest.fixture(scope="module")
+def driving():
+    return synth.named("driving")
+
+
+@pytest.fixture(scope="module")
+def driving_p75(driving):
+    say("prepare driving p=0.75 rank 512")
+    return prep(driving, 512, 0.75)
+
+
+def test_driving_early_levels_match_independent_oracle(driving, driving_p75):
+    """K <= 24 lies inside the chain-agreement horizon: the oracle prepares
+    its own factors."""
+    levels = [1, 2, 8, 24]
+    say("driving p=0.75 levels", levels, "vs oracle-prepared factors")
+    f = oracle.prepare(driving.W, 512, 24, 640)
+    h, _ = run_gpu(driving_p75, driving.x, levels)
+    ho, _ = oracle.run(f, driving.b, driving.x, levels)
+    for j, K in enumerate(levels):
+        assert rel_err(h[j], ho[j]) < TOL, (K, rel_err(h[j], ho[j]))
+
+
+def test_driving_all_budgets_match_oracle_on_exported_terms(driving, driving_p75):
+    levels = [32, 64, 128, 256, 512]
+    say("driving p=0.75 levels", levels, "vs oracle on exported terms")
+    f = exported_factors(driving_p75)
+    h, _ = run_gpu(driving_p75, driving.x, levels)
+    ho, _ = oracle.run(f, driving.b, driving.x, levels)
+    for j, K in enumerate(levels):
+        assert rel_err(h[j], ho[j]) < TOL, (K, rel_err(h[j], ho[j]))
+
+
+def test_driving_levels_are_bitwise_independent(driving, driving_p75):
+    say("driving level independence")
+    together, _ = run_gpu(driving_p75, driving.x, [512, 1, 64])
+    for j, K in enumerate([512, 1, 64]):
+        alone, _ = run_gpu(driving_p75, driving.x, [K])
+        assert np.array_equal(together[j], alone[0]), K
+
+
+def test_driving_full_rank_without_pruning_is_the_exact_lstm(driving):
+    say("driving p=0 rank 512 vs exact LSTM")
+    m = prep(driving, 512, 0.0)
+    h, _ = run_gpu(m, driving.x, [512])
+    he, _ = oracle.exact_lstm(driving.W, driving.b, driving.x)
+    assert rel_err(h[0], he) < TOL
