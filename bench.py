@@ -47,6 +47,7 @@ def main():
     ap.add_argument("--blocks", type=int, default=0, help="workgroups of the run kernel (0 = automatic)")
     ap.add_argument("--sweep", default="1,2,4,8,16,32,64,128,256,512")
     ap.add_argument("--sweep-steps", type=int, default=50)
+    ap.add_argument("--blocks-sweep", default="", help="comma list of workgroup counts to time at K (tuning)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     args = ap.parse_args()
@@ -72,7 +73,7 @@ def main():
     info = m.info
     NZ, G, Rg = info["nz"], info["groups"], info["rows_per_group"]
     if args.blocks:
-        B.approx_lstm_set_launch(m, args.blocks)
+        B.approx_lstm_set_launch(m, args.blocks, 0)
     B.approx_lstm_reserve(m, T, Bn, 1)
     x = torch.from_numpy(wl.x).to(dev)
     h_out = torch.empty((1, T, Bn, H), device=dev)
@@ -108,6 +109,29 @@ def main():
         sweep["timesteps_per_s"].append(round(T * Bn / (msk * 1e-3), 1))
         sweep["hbm_frac"].append(round(byts / (msk * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
 
+    tune = None
+    if args.blocks_sweep:
+        tune = {"K": K, "blocks": [], "us_per_timestep": []}
+        for P in [int(s) for s in args.blocks_sweep.split(",") if s]:
+            B.approx_lstm_set_launch(m, P, 0)
+            tune["blocks"].append(P)
+            tune["us_per_timestep"].append(round(timed(K, args.sweep_steps, 5) * 1e3 / T, 4))
+        B.approx_lstm_set_launch(m, args.blocks, 0)
+
+    # in-kernel phase timing of one run per K (workgroup 0's stamps)
+    phases = {}
+    for k in sorted({1, 64, K}):
+        B.approx_lstm_set_timing(m, 1)
+        B.approx_lstm_run(m, x, [k], h_out, stream=stream)
+        st = B.approx_lstm_get_timing(m, T, stream=stream)
+        B.approx_lstm_set_timing(m, 0)
+        ph = np.array([[st[1 + 4 * t + i] for i in range(4)] + [st[1 + 4 * (t + 1)]] for t in range(T)])
+        phases[str(k)] = {"phaseA_us": round(float(np.mean(ph[:, 1] - ph[:, 0])), 3),
+                          "z_wait_us": round(float(np.mean(ph[:, 2] - ph[:, 1])), 3),
+                          "phaseB_us": round(float(np.mean(ph[:, 3] - ph[:, 2])), 3),
+                          "h_out_us": round(float(np.mean(ph[:, 4] - ph[:, 3])), 3),
+                          "recurrence_us": round(float(st[1 + 4 * T] - st[1]), 3)}
+
     bytes_launch = T * algorithmic_bytes_per_timestep(G, Rg, NZ, C, K, D, H, Bn, 1)
     achieved = bytes_launch / (ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -128,7 +152,7 @@ def main():
                                f"{int(args.prune * 100)}% pruning (NZ={NZ}), K={K}",
                    "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
         "us_per_timestep": round(us_per_ts, 4), "prepare_s": round(prep_s, 2),
-        "sweep": sweep, "roofline": roofline, "cpu_baseline": cpu,
+        "phases": phases, "sweep": sweep, "tune": tune, "roofline": roofline, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 

@@ -149,12 +149,32 @@ approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int3
 approx_lstm_status approx_lstm_check(approx_lstm_model* m, void* hip_stream);
 
 /*
- * approx_lstm_set_launch -- number of workgroups the run kernel uses
- * (0 = automatic: about one per 16 terms in use, at most 128 and at most the
- * device's compute units).  Takes effect on the next run; a tuning knob, the
- * results do not depend on it beyond float32 summation order.
+ * approx_lstm_set_launch -- launch shape of the run kernel, from the next run
+ * on.  blocks: workgroups (0 = automatic: about one per 32 terms in use, at
+ * most 64, widened until the per-workgroup slices fit in LDS; at most the
+ * device's compute units).  The results do not depend on it: every sum has a
+ * fixed order.  cooperative != 0 launches through the cooperative-launch API,
+ * which has the runtime guarantee that all workgroups are resident at once
+ * (about 17 us more per launch); the default plain launch relies on the
+ * device being otherwise idle enough to hold them, and if it is not, the
+ * kernel's bounded waits expire and approx_lstm_check reports
+ * APPROX_LSTM_ERR_DEVICE instead of hanging.
  */
-approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks);
+approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks, int32_t cooperative);
+
+/*
+ * approx_lstm_set_timing -- enable (1) or disable (0) per-timestep device
+ * timestamps in later runs (one device wall-clock read per phase by
+ * workgroup 0; negligible cost).
+ *
+ * approx_lstm_get_timing -- synchronise hip_stream and copy the stamps of the
+ * last run that recorded them, in microseconds from the start of its
+ * recurrence, to host stamps_us[n], n >= 2 + 4T: [0] = 0, then for each
+ * timestep t the starts of phase A (h-part dots), of the z wait, of the U
+ * accumulation and of the h wait at [1+4t .. 4+4t], and the end at [1+4T].
+ */
+approx_lstm_status approx_lstm_set_timing(approx_lstm_model* m, int32_t enable);
+approx_lstm_status approx_lstm_get_timing(approx_lstm_model* m, void* hip_stream, double* stamps_us, int32_t n);
 
 /* approx_lstm_model_info -- sizes, live ranks and device footprint (host struct). */
 approx_lstm_status approx_lstm_model_info(const approx_lstm_model* m, approx_lstm_info* out);

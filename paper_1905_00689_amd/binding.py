@@ -59,8 +59,10 @@ _sigs = {
     "approx_lstm_run": [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp],
     "approx_lstm_reserve": [_vp, _i32, _i32, _i32],
     "approx_lstm_check": [_vp, _vp],
-    "approx_lstm_set_launch": [_vp, _i32],
+    "approx_lstm_set_launch": [_vp, _i32, _i32],
     "approx_lstm_model_info": [_vp, ctypes.POINTER(Info)],
+    "approx_lstm_set_timing": [_vp, _i32],
+    "approx_lstm_get_timing": [_vp, _vp, _vp, _i32],
     "approx_lstm_get_factors": [_vp, _i32, _vp, _vp, _vp, _vp],
     "approx_lstm_get_factors_f64": [_vp, _i32, _vp, _vp, _vp],
 }
@@ -159,8 +161,19 @@ def approx_lstm_check(model, stream=None):
     return _check(lib.approx_lstm_check(model.handle, ctypes.c_void_p(_stream(stream))))
 
 
-def approx_lstm_set_launch(model, blocks):
-    return _check(lib.approx_lstm_set_launch(model.handle, int(blocks)))
+def approx_lstm_set_launch(model, blocks, cooperative=0):
+    return _check(lib.approx_lstm_set_launch(model.handle, int(blocks), int(cooperative)))
+
+
+def approx_lstm_set_timing(model, enable):
+    return _check(lib.approx_lstm_set_timing(model.handle, int(enable)))
+
+
+def approx_lstm_get_timing(model, T, stream=None):
+    """Stamps of the last timed run, microseconds: array [2 + 4T]."""
+    out = np.zeros(2 + 4 * T)
+    _check(lib.approx_lstm_get_timing(model.handle, ctypes.c_void_p(_stream(stream)), out.ctypes.data, out.size))
+    return out
 
 
 def approx_lstm_model_info(model):

@@ -84,6 +84,7 @@ struct approx_lstm_model {
   uint16_t* d_nx = nullptr;
   uint64_t dev_bytes = 0;
   int num_cu = 0;
+  std::vector<int> hpre;             // [N*G] max over terms 0..tau of the h-part entry count
   // run workspace
   float* d_px = nullptr;
   size_t px_cap = 0;                 // floats
@@ -92,11 +93,16 @@ struct approx_lstm_model {
   unsigned long long* d_hx = nullptr;
   size_t hx_cap = 0;
   unsigned* d_err = nullptr;
+  unsigned long long* d_stamps = nullptr;
+  size_t stamps_cap = 0;             // words
+  int timing = 0;                    // record per-timestep stamps
+  int last_T = 0;                    // T of the last run that recorded stamps
   unsigned seq = 0;
   int launch_blocks = 0;             // 0 = automatic
+  int cooperative = 0;               // 1: cooperative launch API
 
   ~approx_lstm_model() {
-    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err) return;
+    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err && !d_stamps) return;
     DeviceScope ds(device);
     dfree(d_sigma);
     dfree(d_Ut);
@@ -108,6 +114,7 @@ struct approx_lstm_model {
     dfree(d_zx);
     dfree(d_hx);
     dfree(d_err);
+    dfree(d_stamps);
   }
 };
 
@@ -152,9 +159,11 @@ approx_lstm_status ensure_workspace(approx_lstm_model* m, size_t px_floats, size
   return APPROX_LSTM_OK;
 }
 
+// Workgroups for a run: about one per 32 terms in use, at most 64 (the
+// tagged all-gather costs ~1.1 us up to 64 workgroups and grows beyond).
 int auto_blocks(const approx_lstm_model* m, int GK) {
-  int cap = std::max(1, std::min(m->num_cu, 128));
-  int want = (GK + 15) / 16;
+  int cap = std::max(1, std::min(m->num_cu, 64));
+  int want = (GK + 31) / 32;
   return std::max(1, std::min(cap, want));
 }
 
@@ -260,6 +269,11 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
         }
         nx_h[tau] = (uint16_t)cnt;
       }
+    m->hpre.resize(NT);
+    for (size_t tau = 0; tau < NT; ++tau) {
+      const int h = nz - nx_h[tau];
+      m->hpre[tau] = tau ? std::max(m->hpre[tau - 1], h) : h;
+    }
     for (int o = 0; o < 4 * H; ++o) {
       const int g = o / Rg, r = o % Rg;
       for (int n = 0; n < N; ++n) Ut_h[(size_t)o * N + n] = m->u[((size_t)g * N + n) * Rg + r];
@@ -313,7 +327,8 @@ approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int3
   DeviceScope ds(m->device);
   if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
   const size_t GK = (size_t)m->G * m->N, LB = (size_t)L_max * B_max;
-  approx_lstm_status st = ensure_workspace(m, GK * T_max * B_max, LB * GK, LB * m->H, nullptr);
+  const size_t P_max = std::max(1, m->num_cu);
+  approx_lstm_status st = ensure_workspace(m, GK * T_max * B_max, LB * (GK + P_max), LB * m->H, nullptr);
   if (st != APPROX_LSTM_OK) return st;
   HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
   return APPROX_LSTM_OK;
@@ -347,25 +362,25 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   a.D = m->D; a.H = m->H; a.G = m->G; a.N = m->N; a.NZ = m->NZ; a.T = T; a.B = B; a.L = n_levels;
   a.GK = m->G * kmax;
   for (int l = 0; l < n_levels; ++l) a.levels[l] = levels[l];
-  const int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, std::max(1, m->num_cu)) : auto_blocks(m, a.GK);
-  a.rows_per = (m->H + P - 1) / P;
+  a.hcap = a.GK > 0 ? m->hpre[a.GK - 1] : 0;
+  a.lanes_a = alstm::lanes_for_terms(m->NZ, m->D, m->H);
+  for (int l = 0; l < n_levels; ++l) a.lanes_b[l] = alstm::lanes_for_level(levels[l]);
+  const int maxP = std::max(1, m->num_cu);
+  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK);
+  size_t lds = alstm::plan_progressive(a, P);
+  if (m->launch_blocks == 0)   // automatic: widen until the per-workgroup slices fit in LDS
+    while (lds > alstm::kLdsCap && P < maxP) {
+      P = std::min(maxP, 2 * P);
+      lds = alstm::plan_progressive(a, P);
+    }
   const size_t LB = (size_t)n_levels * B;
-  const size_t lds_cap = 160 * 1024;
-  // largest (t, b) chunk of x that fits next to the rest of the LDS layout
-  a.xchunk = 1;
-  {
-    alstm::RunArgs probe = a;
-    probe.xchunk = 1;
-    const size_t fixed = alstm::progressive_lds_bytes(probe) - sizeof(float) * std::max<size_t>(m->D, a.GK);
-    const size_t room = lds_cap > fixed ? (lds_cap - fixed) / (sizeof(float) * m->D) : 0;
-    a.xchunk = (int)std::max<size_t>(1, std::min<size_t>({room, (size_t)alstm::kMaxXChunk, (size_t)T * B}));
-  }
-  if (alstm::progressive_lds_bytes(a) > lds_cap)
+  if (lds > alstm::kLdsCap)
     return fail(APPROX_LSTM_ERR_UNSUPPORTED, "LDS need %zu bytes exceeds 160 KiB (H=%d, levels*B=%zu, G*K=%d)",
-                alstm::progressive_lds_bytes(a), m->H, LB, a.GK);
+                lds, m->H, LB, a.GK);
 
   approx_lstm_status st =
-      ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * a.GK), LB * m->H, stream);
+      ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * P * a.owned_max),
+                       LB * m->H, stream);
   if (st != APPROX_LSTM_OK) return st;
   m->seq = (m->seq + 1) & 0xFFFFu;
   if (m->seq == 0) {
@@ -378,7 +393,20 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
   a.sigma = m->d_sigma; a.Ut = m->d_Ut; a.vidx = m->d_vidx; a.vval = m->d_vval; a.nx = m->d_nx;
   a.bias = m->d_bias; a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx; a.err = m->d_err;
-  HIP_TRY(alstm::launch_progressive(a, P, stream), "launch progressive_lstm_kernel");
+  a.stamps = nullptr;
+  if (m->timing) {
+    const size_t words = 4 + 4 * (size_t)T;
+    if (words > m->stamps_cap) {
+      HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+      dfree(m->d_stamps);
+      m->stamps_cap = 0;
+      HIP_TRY(hipMalloc(&m->d_stamps, words * 8), "hipMalloc(stamps)");
+      m->stamps_cap = words;
+    }
+    a.stamps = m->d_stamps;
+    m->last_T = T;
+  }
+  HIP_TRY(alstm::launch_progressive(a, P, m->cooperative, stream), "launch progressive_lstm_kernel");
   return APPROX_LSTM_OK;
 }
 
@@ -399,10 +427,42 @@ approx_lstm_status approx_lstm_check(approx_lstm_model* m, void* hip_stream) {
   return APPROX_LSTM_OK;
 }
 
-approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks) {
+approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks, int32_t cooperative) {
   g_last_error.clear();
   if (!m || blocks < 0) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
   m->launch_blocks = blocks;
+  m->cooperative = cooperative ? 1 : 0;
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_set_timing(approx_lstm_model* m, int32_t enable) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  m->timing = enable ? 1 : 0;
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_get_timing(approx_lstm_model* m, void* hip_stream, double* stamps_us, int32_t n) {
+  g_last_error.clear();
+  if (!m || !stamps_us) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null pointer argument");
+  if (!m->d_stamps || m->last_T <= 0) return fail(APPROX_LSTM_ERR_INVALID_ARG, "no run recorded timing");
+  const int T = m->last_T;
+  const int words = 4 + 4 * T;
+  if (n < 2 + 4 * T) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need %d slots", 2 + 4 * T);
+  DeviceScope ds(m->device);
+  HIP_TRY(hipStreamSynchronize((hipStream_t)hip_stream), "hipStreamSynchronize");
+  std::vector<unsigned long long> raw(words);
+  HIP_TRY(hipMemcpy(raw.data(), m->d_stamps, words * 8, hipMemcpyDeviceToHost), "read stamps");
+  int khz = 0;
+  HIP_TRY(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, m->device), "wall clock rate");
+  if (khz <= 0) return fail(APPROX_LSTM_ERR_DEVICE, "device reports no wall clock rate");
+  // shader-clock stamps, converted with the wall-clock span of the same run
+  const double wall_us = (double)(long long)(raw[3 + 4 * T] - raw[0]) * 1e3 / khz;
+  const double clk = (double)(long long)(raw[2 + 4 * T] - raw[1]);
+  const double us_per_clk = clk > 0 ? wall_us / clk : 0.0;
+  stamps_us[0] = 0.0;
+  for (int i = 0; i < 4 * T; ++i) stamps_us[1 + i] = (double)(long long)(raw[2 + i] - raw[1]) * us_per_clk;
+  stamps_us[1 + 4 * T] = (double)(long long)(raw[2 + 4 * T] - raw[1]) * us_per_clk;
   return APPROX_LSTM_OK;
 }
 

@@ -1,12 +1,14 @@
 // gfx950 kernels for progressive approximate-LSTM inference
 // (arXiv 1905.00689, Sec. III Eq. (1) per gate, then the Sec. II cell update).
 //
-// One cooperative, persistent launch runs a whole sequence.  Workgroup j of P
-// owns the refinement terms tau = j, j+P, j+2P, ... (round-robin, so every
-// prefix K is spread over all workgroups) and a contiguous slice of hidden
-// units.  Per timestep:
-//   phase A  for each owned term: s = P_x + prune(v)_h . h_{t-1};  z = sigma*s
-//            (the x-part P_x was computed for all timesteps in the prologue);
+// One persistent launch runs a whole sequence.  Workgroup j of P owns the
+// refinement terms tau = j, j+P, j+2P, ... (round-robin, so every prefix K is
+// spread over all workgroups) and a contiguous slice of hidden units (all
+// four gates of each).  The prologue computes the x-part projections of the
+// owned terms for every timestep (they do not depend on h) and copies the
+// owned terms' h-part entries, sigma and the owned rows of U into LDS, where
+// they stay for the whole sequence.  Per timestep:
+//   phase A  for each owned term: s = P_x + prune(v)_h . h_{t-1};  z = sigma*s;
 //            z is published as a tagged 64-bit word;
 //   phase B  gather every z of the level, accumulate y = b + sum_n z_n u_n for
 //            the owned rows of all four gates, apply the gate nonlinearities
@@ -14,19 +16,51 @@
 //   phase C  gather the full h_t for the next timestep.
 // The exchanges use relaxed agent-scope 64-bit atomics whose upper half is a
 // per-launch, per-timestep tag: a reader spins until the tag it expects
-// appears, so no counter barrier and no cache-flushing fence is needed.
+// appears, so there is no counter barrier and no cache-flushing fence.  Every
+// wait is bounded; on expiry the kernel records an error and drains.
 #include "kernels.hpp"
+
+#include <algorithm>
 
 namespace alstm {
 
 namespace {
 
 constexpr int kWaves = kThreads / 64;
-constexpr unsigned kSpinLimit = 1u << 21;   // ~1 s at the polling interval below
+constexpr unsigned kSpinLimit = 1u << 21;   // about a second at the polling interval below
+constexpr int kGatherSlots = 8;             // tagged words per thread per gather pass
 
+// Sum over aligned groups of S lanes (S = 1, 2, 4, 8, 16) with DPP lane
+// moves: quad swaps (xor 1, xor 2), then half-row and row mirrors.  Every
+// lane of a group ends with the group's sum; the association order is fixed.
+template <int S>
+__device__ __forceinline__ float group_sum(float v) {
+  if constexpr (S >= 2)
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+  if constexpr (S >= 4)
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
+  if constexpr (S >= 8)
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x141, 0xF, 0xF, false));
+  if constexpr (S >= 16)
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x140, 0xF, 0xF, false));
+  return v;
+}
+
+__device__ __forceinline__ float group_sum_rt(float v, int S) {
+  switch (S) {
+    case 1: return v;
+    case 2: return group_sum<2>(v);
+    case 4: return group_sum<4>(v);
+    case 8: return group_sum<8>(v);
+    default: return group_sum<16>(v);
+  }
+}
+
+// Full-wave sum (input projection): 16-lane rows, then across the 4 rows.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  v = group_sum<16>(v);
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
   return v;
 }
 
@@ -35,85 +69,243 @@ __device__ __forceinline__ void publish(unsigned long long* p, float v, unsigned
   __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Spin until *p carries `tag`, then return its value.  Every wait is bounded:
-// past the limit (or once another wait has failed) it records the failure in
-// *err and returns 0 so that the grid drains.
-__device__ __forceinline__ float await_tagged(const unsigned long long* p, unsigned tag, unsigned* err) {
-  unsigned long long w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  unsigned spins = 0;
-  while ((unsigned)(w >> 32) != tag) {
-    __builtin_amdgcn_s_sleep(1);
-    ++spins;
-    if ((spins & 255u) == 0u) {
-      if (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) {
-        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return 0.0f;
-      }
-    }
-    w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  return __uint_as_float((unsigned)w);
+__device__ __forceinline__ unsigned long long load_tagged(const unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ float sigmoidf_(float z) {
-  // 1/(1+e^-z), written so that the exponential never overflows
-  if (z >= 0.0f) return 1.0f / (1.0f + expf(-z));
-  float e = expf(z);
-  return e / (1.0f + e);
+// Gather of tagged exchange words by threads tid < nthr: word i (< n) lands
+// at dst[map ? map[i] : i] once it carries `tag`.  Each thread keeps two
+// generations of loads of its words in flight (re-issued unconditionally, so
+// the in-order completion counter lets one generation be consumed while the
+// next travels), which halves the delay between a word's arrival and its
+// detection.  Bounded: past the spin limit, or once another wait has failed,
+// it records the failure and stores 0.
+template <int NS>
+__device__ void gather_tagged(float* dst, const uint16_t* map, const unsigned long long* src, int n, unsigned tag,
+                              unsigned* err, int tid, int nthr) {
+  for (int base = 0; base < n; base += nthr * NS) {
+    const unsigned long long* sp[NS];
+    unsigned pending = 0;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      const int i = base + k * nthr + tid;
+      sp[k] = src + (i < n ? i : 0);
+      if (i < n) pending |= 1u << k;
+    }
+    unsigned long long wa[NS], wb[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) wa[k] = load_tagged(sp[k]);
+    __builtin_amdgcn_s_sleep(4);
+#pragma unroll
+    for (int k = 0; k < NS; ++k) wb[k] = load_tagged(sp[k]);
+    unsigned spins = 0;
+    while (true) {
+#pragma unroll
+      for (int k = 0; k < NS; ++k) {
+        if (((pending >> k) & 1u) && (unsigned)(wa[k] >> 32) == tag) {
+          const int i = base + k * nthr + tid;
+          dst[map ? map[i] : i] = __uint_as_float((unsigned)wa[k]);
+          pending &= ~(1u << k);
+        }
+      }
+      if (!pending) break;
+#pragma unroll
+      for (int k = 0; k < NS; ++k) wa[k] = load_tagged(sp[k]);
+#pragma unroll
+      for (int k = 0; k < NS; ++k) {
+        if (((pending >> k) & 1u) && (unsigned)(wb[k] >> 32) == tag) {
+          const int i = base + k * nthr + tid;
+          dst[map ? map[i] : i] = __uint_as_float((unsigned)wb[k]);
+          pending &= ~(1u << k);
+        }
+      }
+      if (!pending) break;
+#pragma unroll
+      for (int k = 0; k < NS; ++k) wb[k] = load_tagged(sp[k]);
+      spins += 2;
+      if ((spins & 254u) == 0u &&
+          (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int k = 0; k < NS; ++k)
+          if ((pending >> k) & 1u) {
+            const int i = base + k * nthr + tid;
+            dst[map ? map[i] : i] = 0.0f;
+          }
+        break;
+      }
+    }
+  }
+}
+
+// z gather of one (level, sequence): exchange slot s carries term
+// tau = slot_term[s]; slots with tau >= GKl are not part of this level (not
+// written this timestep) and are skipped.  z of tau = n*G + g lands at
+// zs[g*Kmax + n].  Same two-generation polling as gather_tagged.
+template <int NS>
+__device__ void gather_level(float* zs, const uint16_t* slot_term, const unsigned long long* src, int nslots,
+                             int GKl, int G, int Kmax, unsigned tag, unsigned* err, int tid, int nthr) {
+  for (int base = 0; base < nslots; base += nthr * NS) {
+    const unsigned long long* sp[NS];
+    int dst[NS];
+    unsigned pending = 0;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      const int s = base + k * nthr + tid;
+      const int tau = s < nslots ? (int)slot_term[s] : GKl;
+      sp[k] = src + (s < nslots ? s : 0);
+      dst[k] = (G == 4) ? ((tau & 3) * Kmax + (tau >> 2)) : tau;
+      if (tau < GKl) pending |= 1u << k;
+    }
+    if (!pending) continue;
+    unsigned long long wa[NS], wb[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) wa[k] = load_tagged(sp[k]);
+    __builtin_amdgcn_s_sleep(4);
+#pragma unroll
+    for (int k = 0; k < NS; ++k) wb[k] = load_tagged(sp[k]);
+    unsigned spins = 0;
+    while (true) {
+#pragma unroll
+      for (int k = 0; k < NS; ++k)
+        if (((pending >> k) & 1u) && (unsigned)(wa[k] >> 32) == tag) {
+          zs[dst[k]] = __uint_as_float((unsigned)wa[k]);
+          pending &= ~(1u << k);
+        }
+      if (!pending) break;
+#pragma unroll
+      for (int k = 0; k < NS; ++k) wa[k] = load_tagged(sp[k]);
+#pragma unroll
+      for (int k = 0; k < NS; ++k)
+        if (((pending >> k) & 1u) && (unsigned)(wb[k] >> 32) == tag) {
+          zs[dst[k]] = __uint_as_float((unsigned)wb[k]);
+          pending &= ~(1u << k);
+        }
+      if (!pending) break;
+#pragma unroll
+      for (int k = 0; k < NS; ++k) wb[k] = load_tagged(sp[k]);
+      spins += 2;
+      if ((spins & 254u) == 0u &&
+          (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int k = 0; k < NS; ++k)
+          if ((pending >> k) & 1u) zs[dst[k]] = 0.0f;
+        break;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void gather_level_any(float* zs, const uint16_t* slot_term, const unsigned long long* src,
+                                                 int nslots, int GKl, int G, int Kmax, unsigned tag, unsigned* err,
+                                                 int tid, int nthr) {
+  const int per = (nslots + nthr - 1) / nthr;     // slots per thread for a single pass
+  if (per <= 1) gather_level<1>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+  else if (per <= 2) gather_level<2>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+  else if (per <= 3) gather_level<3>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+  else if (per <= 5) gather_level<5>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+  else gather_level<8>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+}
+
+// Workgroup barrier that orders LDS only.  __syncthreads() would also wait
+// for every outstanding global store of the wave (gfx9 counts stores in
+// vmcnt), i.e. for the agent-scope exchange stores to reach memory.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Gate nonlinearities from the exponential: sigmoid(z) = 1/(1+e^-z) and
+// tanh(x) = 2 sigmoid(2x) - 1, with the hardware exp2 and reciprocal
+// (relative error ~1e-6 for |z| < 20, exact limits 0 and 1 beyond).
+__device__ __forceinline__ float sigmoid_fast(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+}
+
+__device__ __forceinline__ float tanh_fast(float x) {
+  return 2.0f * sigmoid_fast(2.0f * x) - 1.0f;
+}
+
+// LDS carve-up shared by the host planner and the kernel (byte offsets).
+struct Layout {
+  size_t zs, hs, ys, bs, cs, zown, hown, sig, pxb, zmap, hval, hidx, us, total;
+};
+
+__host__ __device__ inline size_t align16(size_t b) { return (b + 15) & ~(size_t)15; }
+
+__host__ __device__ inline Layout layout_of(const RunArgs& a) {
+  Layout l;
+  const size_t LB = (size_t)a.L * a.B;
+  const size_t kmax = a.G > 0 ? (size_t)a.GK / a.G : 0;
+  size_t o = 0;
+  l.zs = o;     o = align16(o + 4 * (a.GK > 1 ? (size_t)a.GK : 1));   // z of one (level, seq), [g][Kmax]
+  l.hs = o;     o = align16(o + 4 * LB * a.H);                        // h_{t-1} per (level, seq)
+  l.ys = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // y of the owned rows
+  l.bs = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // bias of the owned rows
+  l.cs = o;     o = align16(o + 4 * LB * a.rows_per);                 // c of the owned rows
+  l.zown = o;   o = align16(o + 4 * LB * (size_t)a.owned_max);        // z of the owned terms
+  l.hown = o;   o = align16(o + 4 * LB * a.rows_per);                 // new h of the owned rows
+  l.sig = o;    o = align16(o + 4 * (size_t)a.owned_max);
+  l.pxb = o;    // P_x of every timestep (px_all) or of this and the next one
+  o = align16(o + 4 * (a.px_all ? (size_t)a.T : 2) * a.B * a.owned_max);
+  l.zmap = o;   o = align16(o + 2 * (size_t)a.owned_max * a.P);        // exchange slot -> term
+  l.hval = o;   o = align16(o + (a.vh_lds ? 4 * (size_t)a.owned_max * a.hcap : 0));
+  l.hidx = o;   o = align16(o + (a.vh_lds ? 2 * (size_t)a.owned_max * a.hcap : 0));
+  l.us = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per * a.ustride);
+  (void)kmax;
+  l.total = o;
+  return l;
 }
 
 }  // namespace
 
+// HPL > 0: each phase-A lane keeps HPL h-part entries of its term in
+// registers (requires <= 32 owned terms and hcap <= 16*HPL); 0: entries in
+// LDS.  UPT > 0: each phase-B thread keeps UPT entries of each of OPT output
+// rows in registers (requires one budget K for all levels, S*UPT >= K and
+// 4*rows_per*S <= 512*OPT); 0: U rows in LDS (ustride > 0) or from global.
+template <int HPL, int OPT, int UPT>
 __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const Layout L = layout_of(a);
   const int P = gridDim.x, j = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int D = a.D, H = a.H, G = a.G, N = a.N, NZ = a.NZ, T = a.T, B = a.B;
-  const int LB = a.L * B, TB = T * B, GK = a.GK, RP = a.rows_per;
+  const int LB = a.L * B, GK = a.GK, RP = a.rows_per, OM = a.owned_max;
+  const int Kmax = GK / G;
   const int r0 = j * RP;
   const int rc = max(0, min(RP, H - r0));               // hidden units owned here
   const int n_owned = (GK > j) ? (GK - j + P - 1) / P : 0;
+  const int outs = 4 * rc;
 
-  // LDS carve-up: [shared: x staging | z of one level] [h per (level, b)] [y] [c]
-  const int shared_floats = max(a.xchunk * D, GK);
-  float* xs = lds;
-  float* zs = lds;
-  float* hs = lds + shared_floats;
-  float* ys = hs + LB * H;
-  float* cs = ys + 4 * RP;
+  float* zs = reinterpret_cast<float*>(lds_raw + L.zs);
+  float* hs = reinterpret_cast<float*>(lds_raw + L.hs);
+  float* ys = reinterpret_cast<float*>(lds_raw + L.ys);
+  float* bs = reinterpret_cast<float*>(lds_raw + L.bs);
+  float* cs = reinterpret_cast<float*>(lds_raw + L.cs);
+  float* zown = reinterpret_cast<float*>(lds_raw + L.zown);
+  float* hown = reinterpret_cast<float*>(lds_raw + L.hown);
+  float* sig = reinterpret_cast<float*>(lds_raw + L.sig);
+  float* pxb = reinterpret_cast<float*>(lds_raw + L.pxb);
+  uint16_t* zmap = reinterpret_cast<uint16_t*>(lds_raw + L.zmap);
+  float* hval = reinterpret_cast<float*>(lds_raw + L.hval);
+  uint16_t* hidx = reinterpret_cast<uint16_t*>(lds_raw + L.hidx);
+  float* us = reinterpret_cast<float*>(lds_raw + L.us);
 
-  // ---- prologue: x-part projections P_x[tau][t*B+b] of the owned terms ----
-  for (int cb = 0; cb < TB; cb += a.xchunk) {
-    const int cnt = min(a.xchunk, TB - cb);
-    for (int i = threadIdx.x; i < cnt * D; i += kThreads) xs[i] = a.x[(size_t)cb * D + i];
-    __syncthreads();
-    for (int i = wave; i < n_owned; i += kWaves) {
-      const int tau = j + i * P;
-      const int ne = a.nx[tau];
-      const uint16_t* vi = a.vidx + (size_t)tau * NZ;
-      const float* vv = a.vval + (size_t)tau * NZ;
-      float acc[kMaxXChunk];
-#pragma unroll
-      for (int c = 0; c < kMaxXChunk; ++c) acc[c] = 0.0f;
-      for (int e = lane; e < ne; e += 64) {
-        const float v = vv[e];
-        const int k = vi[e];
-#pragma unroll
-        for (int c = 0; c < kMaxXChunk; ++c)
-          if (c < cnt) acc[c] += v * xs[c * D + k];
-      }
-#pragma unroll
-      for (int c = 0; c < kMaxXChunk; ++c) {
-        if (c < cnt) {
-          const float s = wave_sum(acc[c]);
-          if (lane == 0) a.px[(size_t)tau * TB + cb + c] = s;
-        }
-      }
-    }
-    __syncthreads();
+  // phase-A lane roles: 16 lanes per term, 4 terms per wave per pass
+  const int sub = lane >> 4, sla = lane & 15;
+  // phase-B thread roles (register path: one output row per S threads)
+  const int S0 = a.lanes_b[0];
+  const int ob = threadIdx.x / S0, slb = threadIdx.x % S0;
+
+  // ---- prologue: owned slices into LDS / registers ----
+  for (int i = threadIdx.x; i < n_owned; i += kThreads) sig[i] = a.sigma[j + i * P];
+  for (int i = threadIdx.x; i < outs; i += kThreads) {
+    const int q = i / rc, rr = i - q * rc;
+    bs[q * RP + rr] = a.bias[q * H + r0 + rr];
   }
-
-  // ---- initial state ----
   for (int i = threadIdx.x; i < LB * H; i += kThreads) {
     const int b = (i / H) % B, r = i % H;
     hs[i] = a.h0 ? a.h0[(size_t)b * H + r] : 0.0f;
@@ -122,69 +314,258 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     const int lb = i / RP, rr = i % RP, b = lb % B;
     cs[i] = (a.c0 && rr < rc) ? a.c0[(size_t)b * H + r0 + rr] : 0.0f;
   }
+  // P_x: every timestep if it fits, else timestep 0 (later ones are prefetched)
+  const int px_steps = a.px_all ? T : 1;
+  for (int i = threadIdx.x; i < px_steps * B * n_owned; i += kThreads) {
+    const int tb = i / n_owned, io = i - tb * n_owned;
+    pxb[tb * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + tb];
+  }
+  // exchange slot s = j'*OM + i' carries term tau = j' + i'*P
+  for (int sl = threadIdx.x; sl < P * OM; sl += kThreads) {
+    const int jj = sl / OM, ii = sl - jj * OM;
+    zmap[sl] = (uint16_t)(jj + ii * P);
+  }
+  float hv[HPL > 0 ? HPL : 1];
+  int hi[HPL > 0 ? HPL : 1];
+  const int ia = wave * 4 + sub;                          // register path: this lane's term
+  if constexpr (HPL > 0) {
+#pragma unroll
+    for (int k = 0; k < HPL; ++k) { hv[k] = 0.0f; hi[k] = 0; }
+    if (ia < n_owned) {
+      const int tau = j + ia * P;
+      const int e0 = a.nx[tau], cnt = NZ - e0;
+      const size_t src = (size_t)tau * NZ + e0;
+#pragma unroll
+      for (int k = 0; k < HPL; ++k) {
+        const int e = sla + 16 * k;
+        if (e < cnt) {
+          hv[k] = a.vval[src + e];
+          hi[k] = (int)a.vidx[src + e] - D;
+        }
+      }
+    }
+  } else if (a.vh_lds) {
+    const int tot = n_owned * a.hcap;
+#pragma unroll 4
+    for (int idx = threadIdx.x; idx < tot; idx += kThreads) {
+      const int i = idx / a.hcap, e = idx - i * a.hcap;
+      const int tau = j + i * P;
+      const int e0 = a.nx[tau];
+      const bool live = e < NZ - e0;
+      const size_t src = (size_t)tau * NZ + e0 + e;
+      hval[idx] = live ? a.vval[src] : 0.0f;
+      hidx[idx] = live ? (uint16_t)(a.vidx[src] - D) : (uint16_t)0;
+    }
+  }
+  // register path: output rows ob + o*(512/S0), o < OPT; for each, the
+  // LDS offsets of its y slot and of its group's z, and UPT entries of u
+  float uv[UPT > 0 ? OPT * UPT : 1];
+  int yslot[OPT > 0 ? OPT : 1], zbase[OPT > 0 ? OPT : 1];
+  if constexpr (UPT > 0) {
+    const int stride_o = kThreads / S0;
+#pragma unroll
+    for (int o = 0; o < OPT; ++o) {
+      const int ol = ob + o * stride_o;
+      yslot[o] = -1;
+      zbase[o] = 0;
+#pragma unroll
+      for (int k = 0; k < UPT; ++k) uv[o * UPT + k] = 0.0f;
+      if (ol < outs) {
+        const int q = ol / rc, rr = ol - q * rc;
+        yslot[o] = q * RP + rr;
+        zbase[o] = ((G == 4) ? q : 0) * Kmax;
+        const float* urow = a.Ut + (size_t)(q * H + r0 + rr) * N;
+#pragma unroll
+        for (int k = 0; k < UPT; ++k) {
+          const int n = slb + S0 * k;
+          if (n < Kmax) uv[o * UPT + k] = urow[n];
+        }
+      }
+    }
+  } else if (a.ustride) {
+    const int tot = outs * Kmax;
+#pragma unroll 4
+    for (int idx = threadIdx.x; idx < tot; idx += kThreads) {
+      const int row = idx / Kmax, n = idx - row * Kmax;
+      const int q = row / rc, rr = row - q * rc;
+      us[(size_t)(q * RP + rr) * a.ustride + n] = a.Ut[(size_t)(q * H + r0 + rr) * N + n];
+    }
+  }
   __syncthreads();
 
+  // A single workgroup running a single recurrence keeps z and h in LDS.
+  const bool local = (P == 1 && LB == 1);
+  // The last wave does every global store of the recurrence (exchange words
+  // and h_out); the other waves do the gathers, so no wave waits on its own
+  // stores before its loads.
+  const bool publisher = wave == kWaves - 1;
+  const int gthr = kThreads - 64;
+
+  // stamps come from the publisher wave, which does the stores anyway
+  const bool stamp = a.stamps && j == 0 && (int)threadIdx.x == kThreads - 64;
+  if (stamp) {
+    a.stamps[0] = wall_clock64();
+    a.stamps[1] = clock64();
+  }
   for (int t = 0; t < T; ++t) {
     const unsigned tag = a.tag_base | (unsigned)(t + 1);
+    const float* pxc = pxb + (a.px_all ? t : (t & 1)) * B * OM;
+    if (stamp) a.stamps[2 + 4 * t] = clock64();
 
-    // ---- phase A: z for the owned terms of every (level, sequence) ----
+    // ---- phase A: z = sigma * (P_x + prune(v)_h . h_{t-1}) for the owned terms ----
     for (int lb = 0; lb < LB; ++lb) {
       const int l = lb / B, b = lb % B;
       const int GKl = G * a.levels[l];
+      const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
       const float* h = hs + lb * H;
-      for (int i = wave; i < n_owned; i += kWaves) {
-        const int tau = j + i * P;
-        if (tau >= GKl) break;
-        const int e0 = a.nx[tau];
-        const uint16_t* vi = a.vidx + (size_t)tau * NZ;
-        const float* vv = a.vval + (size_t)tau * NZ;
-        float acc = 0.0f;
-        for (int e = e0 + lane; e < NZ; e += 64) acc += vv[e] * h[vi[e] - D];
-        acc = wave_sum(acc);
-        if (lane == 0) {
-          const float z = a.sigma[tau] * (a.px[(size_t)tau * TB + t * B + b] + acc);
-          publish(a.zx + (size_t)lb * GK + tau, z, tag);
+      if constexpr (HPL > 0) {
+        if (wave * 4 < nl) {
+          float hg[HPL];
+#pragma unroll
+          for (int k = 0; k < HPL; ++k) hg[k] = h[hi[k]];
+          float acc = 0.0f;
+#pragma unroll
+          for (int k = 0; k < HPL; ++k) acc += hv[k] * hg[k];
+          acc = group_sum<16>(acc);
+          if (sla == 0 && ia < nl) {
+            const float z = sig[ia] * (pxc[b * OM + ia] + acc);
+            const int tau = j + ia * P;
+            if (local) zs[(tau % G) * Kmax + tau / G] = z;
+            else zown[lb * OM + ia] = z;
+          }
+        }
+      } else {
+        for (int base = wave * 4; base < nl; base += kWaves * 4) {
+          const int i = base + sub;
+          float acc = 0.0f;
+          if (i < nl) {
+            const float* hvp = hval + i * a.hcap;
+            const uint16_t* hip = hidx + i * a.hcap;
+#pragma unroll 4
+            for (int e = sla; e < a.hcap; e += 16) acc += hvp[e] * h[hip[e]];
+          }
+          acc = group_sum<16>(acc);
+          if (sla == 0 && i < nl) {
+            const float z = sig[i] * (pxc[b * OM + i] + acc);
+            const int tau = j + i * P;
+            if (local) zs[(tau % G) * Kmax + tau / G] = z;
+            else zown[lb * OM + i] = z;
+          }
+        }
+      }
+    }
+    lds_barrier();
+    if (stamp) a.stamps[3 + 4 * t] = clock64();
+    if (publisher && !local) {
+      for (int lb = 0; lb < LB; ++lb) {
+        const int GKl = G * a.levels[lb / B];
+        const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
+        for (int i = lane; i < nl; i += 64)
+          publish(a.zx + (size_t)lb * P * OM + j * OM + i, zown[lb * OM + i], tag);
+      }
+    }
+
+    // ---- phase B: y = b + sum_n z_n u_n for the owned rows, gates, c and h ----
+    if (rc > 0) {
+      for (int lb = 0; lb < LB; ++lb) {
+        const int l = lb / B;
+        const int Kl = a.levels[l];
+        if (!local && !publisher) {
+          // P_x of the next timestep travels while the z words are awaited
+          if (!a.px_all && lb == 0 && t + 1 < T) {
+            float* pxn = pxb + ((t + 1) & 1) * B * OM;
+            for (int i = threadIdx.x; i < B * n_owned; i += gthr) {
+              const int b = i / n_owned, io = i - b * n_owned;
+              pxn[b * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + (t + 1) * B + b];
+            }
+          }
+          // every slot of the exchange whose term is in this level (slots of
+          // workgroups that own fewer terms are skipped by the map check)
+          const int nslots = P * OM;
+          const int GKl = G * Kl;
+          gather_level_any(zs, zmap, a.zx + (size_t)lb * P * OM, nslots, GKl, G, Kmax, tag, a.err, threadIdx.x, gthr);
+        }
+        lds_barrier();
+        if (stamp && lb == 0) a.stamps[4 + 4 * t] = clock64();
+        if constexpr (UPT > 0) {
+          // branch-free: entries past the budget multiply a valid z by 0
+#pragma unroll
+          for (int o = 0; o < OPT; ++o) {
+            // all z reads first (independent LDS loads in flight), then the FMAs
+            float zv[UPT];
+#pragma unroll
+            for (int k = 0; k < UPT; ++k) {
+              const int n = slb + S0 * k;
+              zv[k] = zs[zbase[o] + (n < Kl ? n : 0)];
+            }
+            float acc = 0.0f;
+#pragma unroll
+            for (int k = 0; k < UPT; ++k) {
+              const int n = slb + S0 * k;
+              acc += (n < Kl ? uv[o * UPT + k] : 0.0f) * zv[k];
+            }
+            acc = group_sum_rt(acc, S0);
+            if (yslot[o] >= 0 && slb == 0) ys[yslot[o]] = acc + bs[yslot[o]];
+          }
+        } else {
+          const int S = a.lanes_b[l], OPP = kThreads / S, os = threadIdx.x / S, sl = threadIdx.x % S;
+          for (int base = 0; base < outs; base += OPP) {
+            const int ol = base + os;
+            float acc = 0.0f;
+            int q = 0, rr = 0;
+            if (ol < outs) {
+              q = ol / rc;
+              rr = ol - q * rc;
+              const float* zg = zs + ((G == 4) ? q : 0) * Kmax;
+              if (a.ustride) {
+                const float* urow = us + (size_t)(q * RP + rr) * a.ustride;
+#pragma unroll 8
+                for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+              } else {
+                const float* urow = a.Ut + (size_t)(q * H + r0 + rr) * N;
+#pragma unroll 8
+                for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+              }
+            }
+            acc = group_sum_rt(acc, S);
+            if (sl == 0 && ol < outs) ys[q * RP + rr] = acc + bs[q * RP + rr];
+          }
+        }
+        lds_barrier();
+        for (int rr = threadIdx.x; rr < rc; rr += kThreads) {
+          const float gi = sigmoid_fast(ys[0 * RP + rr]);
+          const float gf = sigmoid_fast(ys[1 * RP + rr]);
+          const float gg = tanh_fast(ys[2 * RP + rr]);
+          const float go = sigmoid_fast(ys[3 * RP + rr]);
+          const float c = gf * cs[lb * RP + rr] + gi * gg;
+          const float hv2 = go * tanh_fast(c);
+          cs[lb * RP + rr] = c;
+          hown[lb * RP + rr] = hv2;
+          if (local) hs[r0 + rr] = hv2;
+        }
+        lds_barrier();
+      }
+    }
+    if (stamp) a.stamps[5 + 4 * t] = clock64();
+    if (publisher) {
+      for (int lb = 0; lb < LB; ++lb) {
+        const int l = lb / B, b = lb % B;
+        for (int rr = lane; rr < rc; rr += 64) {
+          const float h2 = hown[lb * RP + rr];
+          const int r = r0 + rr;
+          a.h_out[(((size_t)l * T + t) * B + b) * H + r] = h2;
+          if (!local) publish(a.hx + (size_t)lb * H + r, h2, tag);
         }
       }
     }
 
-    // ---- phase B: y for the owned rows, gates, c and h ----
-    for (int lb = 0; lb < LB; ++lb) {
-      const int l = lb / B, b = lb % B;
-      const int Kl = a.levels[l];
-      const int GKl = G * Kl;
-      for (int i = threadIdx.x; i < GKl; i += kThreads)
-        zs[i] = await_tagged(a.zx + (size_t)lb * GK + i, tag, a.err);
-      __syncthreads();
-      for (int ol = wave; ol < 4 * rc; ol += kWaves) {
-        const int q = ol / rc, rr = ol % rc;
-        const int o = q * H + r0 + rr;                  // row of the 4H gate stack
-        const int g = (G == 4) ? q : 0;
-        const float* urow = a.Ut + (size_t)o * N;
-        float acc = 0.0f;
-        for (int n = lane; n < Kl; n += 64) acc += zs[n * G + g] * urow[n];
-        acc = wave_sum(acc);
-        if (lane == 0) ys[q * RP + rr] = acc + a.bias[o];
-      }
-      __syncthreads();
-      for (int rr = threadIdx.x; rr < rc; rr += kThreads) {
-        const float gi = sigmoidf_(ys[0 * RP + rr]);
-        const float gf = sigmoidf_(ys[1 * RP + rr]);
-        const float gg = tanhf(ys[2 * RP + rr]);
-        const float go = sigmoidf_(ys[3 * RP + rr]);
-        const float c = gf * cs[lb * RP + rr] + gi * gg;
-        const float hv = go * tanhf(c);
-        cs[lb * RP + rr] = c;
-        const int r = r0 + rr;
-        a.h_out[(((size_t)l * T + t) * B + b) * H + r] = hv;
-        publish(a.hx + (size_t)lb * H + r, hv, tag);
-      }
-      __syncthreads();
-    }
-
     // ---- phase C: gather h_t ----
-    for (int i = threadIdx.x; i < LB * H; i += kThreads) hs[i] = await_tagged(a.hx + i, tag, a.err);
-    __syncthreads();
+    if (!local && !publisher) gather_tagged<2>(hs, nullptr, a.hx, LB * H, tag, a.err, threadIdx.x, gthr);
+    lds_barrier();
+  }
+  if (stamp) {
+    a.stamps[2 + 4 * T] = clock64();
+    a.stamps[3 + 4 * T] = wall_clock64();
   }
 
   if (a.c_out) {
@@ -195,26 +576,283 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
   }
 }
 
+// x-part projections P_x[tau][t*B+b] = prune(v_tau)[k<D] . x_t[b] for every
+// term in use and every (t, b).  They do not depend on h, so they are taken
+// off the recurrence (the x part holds most of each term's non-zeros) and
+// spread over the GPU: each wave takes one term and each workgroup stages a
+// chunk of x transposed in LDS, xt[k][c] with a padded
+// row of xrow floats, so that one entry's values for every (t, b) of the
+// chunk are adjacent.  The term's entries are read once from HBM.
+__global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xchunk, int xrow) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  float* xt = reinterpret_cast<float*>(lds_raw);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int TB = a.T * a.B, D = a.D, NZ = a.NZ;
+  // the wave's term's first 64*kProjEntries x-part entries sit in registers,
+  // loaded (unconditionally, masked afterwards) before x is staged so that
+  // their HBM latency overlaps the staging
+  constexpr int kProjTerms = 1, kProjEntries = 16;
+  int ne[kProjTerms];
+  float ev[kProjTerms][kProjEntries];
+  int ek[kProjTerms][kProjEntries];
+#pragma unroll
+  for (int w = 0; w < kProjTerms; ++w) {
+    const int tau = (blockIdx.x * kWaves + wave) * kProjTerms + w;
+    const int tc = tau < a.GK ? tau : 0;
+    const uint16_t* vi = a.vidx + (size_t)tc * NZ;
+    const float* vv = a.vval + (size_t)tc * NZ;
+#pragma unroll
+    for (int q = 0; q < kProjEntries; ++q) {
+      const int e = min(lane + 64 * q, NZ - 1);
+      ev[w][q] = vv[e];
+      ek[w][q] = vi[e];
+    }
+    ne[w] = tau < a.GK ? (int)a.nx[tau] : 0;
+  }
+#pragma unroll
+  for (int w = 0; w < kProjTerms; ++w)
+#pragma unroll
+    for (int q = 0; q < kProjEntries; ++q)
+      if (lane + 64 * q >= ne[w]) {
+        ev[w][q] = 0.0f;
+        ek[w][q] = 0;
+      }
+  for (int cb = 0; cb < TB; cb += xchunk) {
+    const int cnt = min(xchunk, TB - cb);
+    __syncthreads();
+    if ((D & 3) == 0 && xchunk == kMaxXChunk) {
+      // lane (c, k4) loads x[cb+c][4k4 .. 4k4+3]; a wave's 64 writes of one
+      // component land in 64 distinct banks (row stride 20 = 16 + 4)
+      const int n = kMaxXChunk * (D >> 2);
+      constexpr int kStage = 8;                            // float4 loads in flight per thread
+      for (int base = 0; base < n; base += kThreads * kStage) {
+        float4 v[kStage];
+#pragma unroll
+        for (int u = 0; u < kStage; ++u) {
+          const int i = base + u * kThreads + (int)threadIdx.x;
+          const int c = i & (kMaxXChunk - 1), k4 = i >> 4;
+          v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (i < n && c < cnt) v[u] = reinterpret_cast<const float4*>(a.x + (size_t)(cb + c) * D)[k4];
+        }
+#pragma unroll
+        for (int u = 0; u < kStage; ++u) {
+          const int i = base + u * kThreads + (int)threadIdx.x;
+          if (i < n) {
+            const int c = i & (kMaxXChunk - 1), k4 = i >> 4;
+            float* d = xt + (4 * k4) * xrow + c;
+            d[0] = v[u].x;
+            d[xrow] = v[u].y;
+            d[2 * xrow] = v[u].z;
+            d[3 * xrow] = v[u].w;
+          }
+        }
+      }
+    } else {
+      for (int c = 0; c < xchunk; ++c)
+        for (int k = threadIdx.x; k < D; k += kThreads)
+          xt[k * xrow + c] = c < cnt ? a.x[(size_t)(cb + c) * D + k] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kProjTerms; ++w) {
+      const int tau = (blockIdx.x * kWaves + wave) * kProjTerms + w;
+      if (tau >= a.GK) break;
+      const uint16_t* vi = a.vidx + (size_t)tau * NZ;
+      const float* vv = a.vval + (size_t)tau * NZ;
+      float acc[kMaxXChunk];
+#pragma unroll
+      for (int c = 0; c < kMaxXChunk; ++c) acc[c] = 0.0f;
+      if (xchunk == kMaxXChunk) {
+#pragma unroll
+        for (int q = 0; q < kProjEntries; ++q) {
+          if (64 * q < ne[w]) {
+            const float v = ev[w][q];
+            const float4* xk = reinterpret_cast<const float4*>(xt + ek[w][q] * xrow);
+#pragma unroll
+            for (int r = 0; r < kMaxXChunk / 4; ++r) {
+              const float4 x4 = xk[r];
+              acc[4 * r + 0] += v * x4.x;
+              acc[4 * r + 1] += v * x4.y;
+              acc[4 * r + 2] += v * x4.z;
+              acc[4 * r + 3] += v * x4.w;
+            }
+          }
+        }
+        for (int e = lane + 64 * kProjEntries; e < ne[w]; e += 64) {
+          const float v = vv[e];
+          const float4* xk = reinterpret_cast<const float4*>(xt + (int)vi[e] * xrow);
+#pragma unroll
+          for (int r = 0; r < kMaxXChunk / 4; ++r) {
+            const float4 x4 = xk[r];
+            acc[4 * r + 0] += v * x4.x;
+            acc[4 * r + 1] += v * x4.y;
+            acc[4 * r + 2] += v * x4.z;
+            acc[4 * r + 3] += v * x4.w;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < kProjEntries; ++q) {
+          if (64 * q < ne[w]) {
+            const float v = ev[w][q];
+            const float* xk = xt + ek[w][q] * xrow;
+#pragma unroll
+            for (int c = 0; c < kMaxXChunk; ++c)
+              if (c < xchunk) acc[c] += v * xk[c];
+          }
+        }
+        for (int e = lane + 64 * kProjEntries; e < ne[w]; e += 64) {
+          const float v = vv[e];
+          const float* xk = xt + (int)vi[e] * xrow;
+#pragma unroll
+          for (int c = 0; c < kMaxXChunk; ++c)
+            if (c < xchunk) acc[c] += v * xk[c];
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < kMaxXChunk; ++c) {
+        if (c < cnt) {
+          const float s = wave_sum(acc[c]);
+          if (lane == 0) a.px[(size_t)tau * TB + cb + c] = s;
+        }
+      }
+    }
+  }
+}
+
 __global__ void clear_u64_kernel(unsigned long long* p, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = 0ull;
 }
 
-size_t progressive_lds_bytes(const RunArgs& a) {
-  const size_t shared_floats = (size_t)std::max(a.xchunk * a.D, a.GK);
-  const size_t LB = (size_t)a.L * a.B;
-  return sizeof(float) * (shared_floats + LB * a.H + 4 * (size_t)a.rows_per + LB * a.rows_per);
+int lanes_for_terms(int nz, int D, int H) {
+  (void)nz; (void)D; (void)H;
+  return 16;   // phase A always reduces over 16 lanes per term
 }
 
-hipError_t launch_progressive(const RunArgs& a, int blocks, hipStream_t stream) {
-  const size_t lds = progressive_lds_bytes(a);
-  hipError_t e = hipFuncSetAttribute((const void*)progressive_lstm_kernel,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  RunArgs copy = a;
-  void* args[] = {&copy};
-  return hipLaunchCooperativeKernel((const void*)progressive_lstm_kernel, dim3(blocks), dim3(kThreads),
-                                    args, (unsigned)lds, stream);
+int lanes_for_level(int K) {
+  // about 32 terms per lane, at most 16 lanes per output row
+  int s = 1;
+  while (s < 16 && 32 * s < K) s <<= 1;
+  return s;
+}
+
+size_t plan_progressive(RunArgs& a, int P) {
+  a.rows_per = (a.H + P - 1) / P;
+  a.owned_max = a.GK > 0 ? (a.GK + P - 1) / P : 0;
+  a.lanes_a = 16;
+  int smax = 1;
+  bool same_s = true;
+  for (int l = 0; l < a.L; ++l) {
+    smax = std::max(smax, a.lanes_b[l]);
+    same_s = same_s && a.lanes_b[l] == a.lanes_b[0];
+  }
+  const int Kmax = a.G > 0 ? a.GK / a.G : 0;
+  // register residency (no LDS needed for those slices)
+  a.hpl = 0;
+  if (a.owned_max <= 4 * kWaves) {
+    const int need = (a.hcap + 15) / 16;
+    for (int c : {4, 8, 12, 16, 24, 32})
+      if (need <= c) { a.hpl = c; break; }
+  }
+  a.upt = 0;
+  a.opt = 0;
+  bool same_k = true;
+  for (int l = 0; l < a.L; ++l) same_k = same_k && a.levels[l] == a.levels[0];
+  if (same_k && same_s && Kmax > 0) {
+    const int S = a.lanes_b[0];
+    const int need_u = (Kmax + S - 1) / S;
+    const int need_o = (4 * a.rows_per * S + kThreads - 1) / kThreads;
+    if (need_o <= 1 && need_u <= 32) { a.opt = 1; a.upt = 32; }
+    else if (need_o <= 2 && need_u <= 16) { a.opt = 2; a.upt = 16; }
+    else if (need_o <= 4 && need_u <= 8) { a.opt = 4; a.upt = 8; }
+    if (a.opt == 1 && need_u <= 8) a.upt = 8;
+    else if (a.opt == 1 && need_u <= 16) a.upt = 16;
+  }
+  a.P = P;
+  a.vh_lds = 0;
+  a.ustride = 0;
+  a.px_all = 0;
+  size_t need = layout_of(a).total;
+  if (need > kLdsCap) return need;
+  if (a.hpl == 0) {
+    a.vh_lds = 1;
+    if (layout_of(a).total > kLdsCap) return layout_of(a).total;   // h-part entries must fit
+  }
+  if (a.upt == 0 && Kmax > 0) {
+    // stride = smax * odd: the lanes of consecutive rows hit distinct banks
+    a.ustride = smax * ((((Kmax + smax - 1) / smax)) | 1);
+    if (layout_of(a).total > kLdsCap) a.ustride = 0;
+  }
+  a.px_all = 1;
+  if (layout_of(a).total > kLdsCap) a.px_all = 0;
+  return layout_of(a).total;
+}
+
+template <int HPL, int OPT, int UPT>
+hipError_t launch_one(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
+  static bool attr_set = false;
+  const void* fn = (const void*)progressive_lstm_kernel<HPL, OPT, UPT>;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsCap);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  if (cooperative) {
+    RunArgs copy = a;
+    void* args[] = {&copy};
+    return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(kThreads), args, (unsigned)lds, stream);
+  }
+  progressive_lstm_kernel<HPL, OPT, UPT><<<dim3(blocks), dim3(kThreads), lds, stream>>>(a);
+  return hipGetLastError();
+}
+
+template <int HPL>
+hipError_t launch_u(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
+  if (a.opt == 1 && a.upt == 8) return launch_one<HPL, 1, 8>(a, blocks, cooperative, lds, stream);
+  if (a.opt == 1 && a.upt == 16) return launch_one<HPL, 1, 16>(a, blocks, cooperative, lds, stream);
+  if (a.opt == 1 && a.upt == 32) return launch_one<HPL, 1, 32>(a, blocks, cooperative, lds, stream);
+  if (a.opt == 2) return launch_one<HPL, 2, 16>(a, blocks, cooperative, lds, stream);
+  if (a.opt == 4) return launch_one<HPL, 4, 8>(a, blocks, cooperative, lds, stream);
+  return launch_one<HPL, 1, 0>(a, blocks, cooperative, lds, stream);
+}
+
+hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hipStream_t stream) {
+  if (a.GK > 0) {
+    // largest chunk of (t, b) pairs whose transposed x fits in LDS (odd row
+    // stride: the lanes' rows fall in different banks)
+    const int TB = a.T * a.B;
+    // full chunks of 16 (t, b) pairs use a 16-byte aligned row of 20 floats;
+    // smaller ones an odd row (the lanes' rows then fall in different banks)
+    int xchunk = kMaxXChunk, xrow = kMaxXChunk + 4;
+    if ((size_t)a.D * xrow * 4 > kLdsCap) {
+      xchunk = kMaxXChunk - 1;
+      while (xchunk > 1 && (size_t)a.D * (xchunk | 1) * 4 > kLdsCap) --xchunk;
+      xrow = xchunk | 1;
+    }
+    const size_t plds = (size_t)a.D * xrow * 4;
+    static bool proj_attr = false;
+    if (!proj_attr) {
+      hipError_t e = hipFuncSetAttribute((const void*)input_proj_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         (int)kLdsCap);
+      if (e != hipSuccess) return e;
+      proj_attr = true;
+    }
+    const int per_block = kWaves;       // one term per wave
+    input_proj_kernel<<<dim3((a.GK + per_block - 1) / per_block), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const size_t lds = layout_of(a).total;
+  switch (a.hpl) {
+    case 4: return launch_u<4>(a, blocks, cooperative, lds, stream);
+    case 8: return launch_u<8>(a, blocks, cooperative, lds, stream);
+    case 12: return launch_u<12>(a, blocks, cooperative, lds, stream);
+    case 16: return launch_u<16>(a, blocks, cooperative, lds, stream);
+    case 24: return launch_u<24>(a, blocks, cooperative, lds, stream);
+    case 32: return launch_u<32>(a, blocks, cooperative, lds, stream);
+    default: return launch_u<0>(a, blocks, cooperative, lds, stream);
+  }
 }
 
 hipError_t launch_clear_u64(unsigned long long* p, size_t n, hipStream_t stream) {

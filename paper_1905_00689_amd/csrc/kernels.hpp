@@ -8,7 +8,8 @@ namespace alstm {
 
 constexpr int kMaxLevels = 16;
 constexpr int kThreads = 512;          // 8 wave64 per workgroup
-constexpr int kMaxXChunk = 16;         // (t, b) pairs staged per prologue pass
+constexpr int kMaxXChunk = 16;         // (t, b) pairs accumulated per pass of the input projection
+constexpr size_t kLdsCap = 160 * 1024; // LDS per CU on gfx950
 
 // Everything one launch of the progressive-LSTM kernel needs.  Device
 // pointers unless noted.  Layouts (row-major):
@@ -20,8 +21,9 @@ constexpr int kMaxXChunk = 16;         // (t, b) pairs staged per prologue pass
 //   vval   [N*G][NZ]            entries of prune(v) on vidx
 //   nx     [N*G] uint16         number of vidx entries < D (the x/h split)
 //   bias   [4H]
-//   px     [GK][T*B]            x-part projections (workspace)
-//   zx     [L*B][GK] u64        tagged z exchange (value | tag << 32)
+//   px     [GK][T*B]            x-part projections (workspace, written by input_proj_kernel)
+//   zx     [L*B][P][owned_max] u64  tagged z exchange (value | tag << 32), slot
+//                                   j*owned_max + i carries term j + i*P
 //   hx     [L*B][H] u64         tagged h exchange
 struct RunArgs {
   const float* x;
@@ -39,19 +41,44 @@ struct RunArgs {
   unsigned long long* zx;
   unsigned long long* hx;
   unsigned* err;
+  unsigned long long* stamps;  // null, or [4 + 4T] stamps written by workgroup 0: [0] wall clock
+                               // and [1] shader clock at the start of the recurrence; shader
+                               // clock at [2+4t..5+4t], the starts of phase A, the z wait, the
+                               // U accumulation and the h wait of timestep t; [2+4T] shader
+                               // clock and [3+4T] wall clock at the end
   int D, H, G, N, NZ, T, B, L;
   int GK;          // G * max level: terms in use
   int rows_per;    // hidden units owned per workgroup
-  int xchunk;      // (t, b) pairs staged per prologue pass (<= kMaxXChunk)
+  int owned_max;   // max terms owned by one workgroup = ceil(GK / P)
+  int hcap;        // slots per owned term for its h-part entries (max over terms of NZ - nx)
+  int hpl;         // h-part entries per lane held in registers (0: in LDS, see vh_lds)
+  int vh_lds;      // 1: owned terms' h-part entries resident in LDS
+  int upt;         // U entries per output row and thread held in registers (0: LDS or global)
+  int opt;         // output rows per thread in the register path
+  int ustride;     // LDS row stride (floats) of the resident U slice; 0 = U read from global
+  int px_all;      // 1: x-part projections of every timestep resident in LDS
+  int P;           // workgroups of the launch
+  int lanes_a;     // lanes per term in phase A (16)
   unsigned tag_base;
   int levels[kMaxLevels];
+  int lanes_b[kMaxLevels];  // lanes per output row in phase B, per level (a function of K only)
 };
 
-// LDS bytes the kernel needs for these sizes.
-size_t progressive_lds_bytes(const RunArgs& a);
+// Reduction shapes.  They depend only on the model (phase A) and on each
+// level's own budget (phase B), never on the launch width or on the other
+// levels of a run, so every result has one fixed summation order.
+int lanes_for_terms(int nz, int D, int H);
+int lanes_for_level(int K);
 
-// Cooperative launch of `blocks` workgroups on `stream`.
-hipError_t launch_progressive(const RunArgs& a, int blocks, hipStream_t stream);
+// Fills the launch-shape fields (rows_per .. lanes_a) for P workgroups and
+// returns the LDS bytes the kernel then needs (> kLdsCap: does not fit).
+size_t plan_progressive(RunArgs& a, int P);
+
+// Launches, on `stream`, the input projection over the whole device and then
+// the persistent recurrence kernel with `blocks` workgroups.  cooperative != 0
+// uses the cooperative launch API for the latter (co-residency checked by the
+// runtime).
+hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hipStream_t stream);
 
 // Zero `n` 64-bit words (exchange-buffer reset) with a plain kernel.
 hipError_t launch_clear_u64(unsigned long long* p, size_t n, hipStream_t stream);

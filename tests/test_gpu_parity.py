@@ -115,9 +115,9 @@ def test_ragged_shapes_and_launch_widths(G):
     m = prep(w, rank, 0.6, G)
     f = oracle.prepare(w.W, 37, rank, oracle.nz_from_ratio(87, 0.6), groups=G)
     ref = None
-    for P in (0, 1, 5, 16, 37, 64):
-        say("  blocks", P)
-        B.approx_lstm_set_launch(m, P)
+    for P, coop in ((0, 0), (1, 0), (5, 0), (16, 1), (37, 0), (64, 0)):
+        say("  blocks", P, "cooperative", coop)
+        B.approx_lstm_set_launch(m, P, coop)
         h, _ = run_gpu(m, w.x, levels)
         ho, _ = oracle.run(f, w.b, w.x, levels)
         assert rel_err(h, ho) < TOL, P
