@@ -49,6 +49,9 @@ def main():
     ap.add_argument("--sweep-steps", type=int, default=50)
     ap.add_argument("--blocks-sweep", default="", help="comma list of workgroup counts to time at K (tuning)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-phases", action="store_true", help="skip the in-kernel phase stamps")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only time a plain 256 MiB device copy (reference for HBM counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     args = ap.parse_args()
 
@@ -58,6 +61,9 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
     from paper_1905_00689_amd import synth
     from paper_1905_00689_amd import binding as B
 
@@ -120,7 +126,7 @@ def main():
 
     # in-kernel phase timing of one run per K (workgroup 0's stamps)
     phases = {}
-    for k in sorted({1, 64, K}):
+    for k in ([] if args.no_phases else sorted({1, 64, K})):
         B.approx_lstm_set_timing(m, 1)
         B.approx_lstm_run(m, x, [k], h_out, stream=stream)
         st = B.approx_lstm_get_timing(m, T, stream=stream)
@@ -132,11 +138,16 @@ def main():
                           "h_out_us": round(float(np.mean(ph[:, 4] - ph[:, 3])), 3),
                           "recurrence_us": round(float(st[1 + 4 * T] - st[1]), 3)}
 
+    # One step launches input_proj_kernel (x-part projections, whole GPU) and
+    # then progressive_lstm_kernel (the recurrence); the roofline covers the
+    # step, timed with events on the launch stream over the timed region.
     bytes_launch = T * algorithmic_bytes_per_timestep(G, Rg, NZ, C, K, D, H, Bn, 1)
     achieved = bytes_launch / (ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": "progressive_lstm_kernel", "bytes_per_launch": bytes_launch,
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic() if (K == 512 and abs(args.prune - 0.75) < 1e-9) else None,
+                "kernel": "one step: input_proj_kernel + progressive_lstm_kernel",
+                "bytes_per_launch": bytes_launch,
                 "flops_per_launch": T * algorithmic_flops_per_timestep(G, Rg, NZ, K, Bn)}
 
     cpu = None
@@ -155,6 +166,42 @@ def main():
         "phases": phases, "sweep": sweep, "tune": tune, "roofline": roofline, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic():
+    """HBM bytes per step from the committed rocprofv3 counter summary, if it
+    was taken on the kernel source as it is now (else None)."""
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    prof = os.path.join(root, "profiles", "driving_K512_p75_hbm_counters.md")
+    src = os.path.join(root, "paper_1905_00689_amd", "csrc", "kernels.hip")
+    try:
+        fields = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if ": " in l and not l.startswith(" "))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if fields.get("kernel_source_sha256", "").strip() != sha:
+            return None
+        return int(fields["traffic_bytes_per_step"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration(torch):
+    """A plain device-to-device copy of 256 MiB, 5 times: its HBM counters per
+    dispatch (read 256 MiB, write 256 MiB) calibrate FETCH_SIZE / WRITE_SIZE."""
+    n = 64 << 20                                   # float32 elements = 256 MiB
+    a = torch.ones(n, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 5
+    print(json.dumps({"copy_bytes_each_way": 4 * n, "ms_per_copy": round(ms, 4),
+                      "gbs_read_plus_write": round(8 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
 def cpu_baseline(m, wl, K, seconds):
