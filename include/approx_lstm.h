@@ -134,6 +134,49 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
                                    int32_t n_levels, float* h_out, float* c_out, void* hip_stream);
 
 /*
+ * approx_lstm_run_deadline -- progressive LSTM under a per-timestep time
+ * budget (the paper's time-constrained setting: the best output reachable
+ * within the budget, Sec. I, and computation cut when the budget is hit,
+ * Sec. VI-B).  Picks the largest K whose measured in-kernel time per timestep
+ * (from the start of one timestep to the start of the next, device clock)
+ * meets deadline_us_per_step and runs the sequence at that K.
+ *
+ *   x, T, B, h0, c0  as for approx_lstm_run (T >= 1)
+ *   h_out            device [T][B][H]
+ *   k_achieved       host [T]: the K used at every timestep
+ *   step_us          host [T] or NULL: measured microseconds of every timestep
+ *
+ * On first use for a (T, B, launch width) the call calibrates time against K
+ * by running the sequence at K = 0, 1, 2, 4, ..., rank (cached in the model),
+ * then bisects between the two calibrated budgets around the deadline with
+ * fresh runs.  Synchronises hip_stream.  Returns
+ * APPROX_LSTM_ERR_DEADLINE_INFEASIBLE if even K = 0 misses the deadline;
+ * individual timesteps of the final run may still exceed it (step_us tells).
+ */
+approx_lstm_status approx_lstm_run_deadline(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                            const float* h0, const float* c0, double deadline_us_per_step,
+                                            float* h_out, int32_t* k_achieved, float* step_us, void* hip_stream);
+
+/*
+ * approx_lstm_run_stack -- stacked LSTM layers, each progressive: layer l
+ * (l >= 1) takes as its input sequence the h_t of layer l-1 at the same level.
+ *
+ *   layers    host [n_layers]: prepared models; layers[l]->input_size must
+ *             equal layers[l-1]->hidden_size; all on one device
+ *   x         device [T][B][D_0]
+ *   levels    host [n_levels][n_layers]: K of every layer at every level
+ *   h_out     device [n_levels][T][B][H_last]
+ *
+ * Initial states are zero.  Intermediate sequences live in a buffer owned by
+ * layers[0] (allocated on first use, which blocks).  Asynchronous on
+ * hip_stream otherwise.  Layers are run one after another; layer 0 runs all
+ * levels in one launch pair, each later layer one launch pair per level.
+ */
+approx_lstm_status approx_lstm_run_stack(approx_lstm_model* const* layers, int32_t n_layers, const float* x,
+                                         int32_t T, int32_t B, const int32_t* levels, int32_t n_levels,
+                                         float* h_out, void* hip_stream);
+
+/*
  * approx_lstm_reserve -- preallocate the run workspace for up to T_max
  * timesteps, B_max sequences and L_max levels, so that later runs within
  * those sizes allocate nothing.  Blocking.

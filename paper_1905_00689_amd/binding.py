@@ -58,6 +58,8 @@ _sigs = {
     "approx_lstm_prepare": [_vp, _vp, _vp, ctypes.POINTER(PrepareParams), _vp, ctypes.POINTER(_vp)],
     "approx_lstm_run": [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp],
     "approx_lstm_reserve": [_vp, _i32, _i32, _i32],
+    "approx_lstm_run_stack": [_vp, _i32, _vp, _i32, _i32, _vp, _i32, _vp, _vp],
+    "approx_lstm_run_deadline": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
     "approx_lstm_check": [_vp, _vp],
     "approx_lstm_set_launch": [_vp, _i32, _i32],
     "approx_lstm_model_info": [_vp, ctypes.POINTER(Info)],
@@ -113,10 +115,10 @@ class Model:
         self.status = status
         self.hidden_size = approx_lstm_model_info(self)["hidden_size"]
 
-    def __del__(self):
+    def __del__(self, _destroy=lib.approx_lstm_destroy):
         h, self.handle = getattr(self, "handle", None), None
         if h:
-            lib.approx_lstm_destroy(h)
+            _destroy(h)
 
     @property
     def info(self):
@@ -150,6 +152,34 @@ def approx_lstm_run(model, x, levels, h_out, h0=None, c0=None, c_out=None, strea
     st = lib.approx_lstm_run(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)), _dev(c0, "c0", (B, H)),
                              lv, len(levels), _dev(h_out, "h_out", (len(levels), T, B, H)),
                              _dev(c_out, "c_out", (len(levels), B, H)), ctypes.c_void_p(_stream(stream)))
+    return _check(st)
+
+
+def approx_lstm_run_deadline(model, x, deadline_us, h_out, h0=None, c0=None, stream=None):
+    """x [T, B, D], h_out [T, B, H] GPU float32.  Returns (k_achieved [T], step_us [T]) numpy arrays."""
+    T, B, D = x.shape
+    H = model.hidden_size
+    k = np.zeros(T, np.int32)
+    us = np.zeros(T, np.float32)
+    st = lib.approx_lstm_run_deadline(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)), _dev(c0, "c0", (B, H)),
+                                      float(deadline_us), _dev(h_out, "h_out", (T, B, H)), k.ctypes.data,
+                                      us.ctypes.data, ctypes.c_void_p(_stream(stream)))
+    _check(st)
+    return k, us
+
+
+def approx_lstm_run_stack(models, x, levels, h_out, stream=None):
+    """models: list of Model; x [T, B, D0]; levels: [n_levels][n_layers] ints;
+    h_out [n_levels, T, B, H_last] GPU float32 tensor."""
+    T, B, D = x.shape
+    nl, L = len(models), len(levels)
+    arr = (ctypes.c_void_p * nl)(*[m.handle for m in models])
+    flat = [int(k) for row in levels for k in row]
+    assert len(flat) == nl * L
+    lv = (ctypes.c_int32 * len(flat))(*flat)
+    H = models[-1].hidden_size
+    st = lib.approx_lstm_run_stack(arr, nl, _dev(x, "x"), T, B, lv, L, _dev(h_out, "h_out", (L, T, B, H)),
+                                   ctypes.c_void_p(_stream(stream)))
     return _check(st)
 
 

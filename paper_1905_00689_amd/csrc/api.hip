@@ -98,11 +98,17 @@ struct approx_lstm_model {
   int timing = 0;                    // record per-timestep stamps
   int last_T = 0;                    // T of the last run that recorded stamps
   unsigned seq = 0;
+  float* d_stack = nullptr;          // intermediate h of stacked runs (owned by the first layer)
+  size_t stack_cap = 0;              // floats
+  // deadline calibration: in-kernel microseconds per timestep against K, for
+  // the (T, B, launch_blocks) it was measured at
+  std::vector<std::pair<int, double>> calib;
+  int calib_T = -1, calib_B = -1, calib_blocks = -1;
   int launch_blocks = 0;             // 0 = automatic
   int cooperative = 0;               // 1: cooperative launch API
 
   ~approx_lstm_model() {
-    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err && !d_stamps) return;
+    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err && !d_stamps && !d_stack) return;
     DeviceScope ds(device);
     dfree(d_sigma);
     dfree(d_Ut);
@@ -115,6 +121,7 @@ struct approx_lstm_model {
     dfree(d_hx);
     dfree(d_err);
     dfree(d_stamps);
+    dfree(d_stack);
   }
 };
 
@@ -159,10 +166,10 @@ approx_lstm_status ensure_workspace(approx_lstm_model* m, size_t px_floats, size
   return APPROX_LSTM_OK;
 }
 
-// Workgroups for a run: about one per 32 terms in use, at most 64 (the
-// tagged all-gather costs ~1.1 us up to 64 workgroups and grows beyond).
+// Workgroups for a run: about one per 32 terms in use (so that every
+// workgroup's terms and rows fit registers), at most 256.
 int auto_blocks(const approx_lstm_model* m, int GK) {
-  int cap = std::max(1, std::min(m->num_cu, 64));
+  int cap = std::max(1, std::min(m->num_cu, 256));
   int want = (GK + 31) / 32;
   return std::max(1, std::min(cap, want));
 }
@@ -210,6 +217,10 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
     }
     alstm::FactoriseOptions opt;
     opt.keep_unpruned = keep;
+    // groups run on their own threads; the rest of the host's cores split the
+    // row loops inside each group
+    const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+    opt.threads = std::max(1, (int)(hw / (unsigned)G));
     std::vector<std::thread> th;
     for (int g = 0; g < G; ++g)
       th.emplace_back([&, g] { alstm::factorise_group(&W[(size_t)g * Rg * C], Rg, C, N, nz, opt, gf[g]); });
@@ -410,6 +421,71 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   return APPROX_LSTM_OK;
 }
 
+approx_lstm_status approx_lstm_run_stack(approx_lstm_model* const* layers, int32_t n_layers, const float* x, int32_t T,
+                                         int32_t B, const int32_t* levels, int32_t n_levels, float* h_out,
+                                         void* hip_stream) {
+  g_last_error.clear();
+  if (!layers || n_layers < 1 || !levels || n_levels < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
+  if (n_levels > APPROX_LSTM_MAX_LEVELS)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "at most %d levels per run", APPROX_LSTM_MAX_LEVELS);
+  if (T < 0 || B < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need T >= 0 and B >= 1");
+  for (int l = 0; l < n_layers; ++l) {
+    if (!layers[l] || !layers[l]->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "layer %d has no device store", l);
+    if (l > 0 && layers[l]->D != layers[l - 1]->H)
+      return fail(APPROX_LSTM_ERR_INVALID_ARG, "layer %d input size %d != layer %d hidden size %d", l, layers[l]->D,
+                  l - 1, layers[l - 1]->H);
+    if (layers[l]->device != layers[0]->device) return fail(APPROX_LSTM_ERR_INVALID_ARG, "layers on different devices");
+    for (int j = 0; j < n_levels; ++j) {
+      const int K = levels[(size_t)j * n_layers + l];
+      if (K < 0 || K > layers[l]->N)
+        return fail(APPROX_LSTM_ERR_INVALID_ARG, "level %d layer %d: K = %d not in [0, %d]", j, l, K, layers[l]->N);
+    }
+  }
+  if (T == 0) return APPROX_LSTM_OK;
+  if (!x || !h_out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null x or h_out");
+  if (n_layers == 1) {
+    std::vector<int32_t> lv(n_levels);
+    for (int j = 0; j < n_levels; ++j) lv[j] = levels[j];
+    return approx_lstm_run(layers[0], x, T, B, nullptr, nullptr, lv.data(), n_levels, h_out, nullptr, hip_stream);
+  }
+  approx_lstm_model* m0 = layers[0];
+  DeviceScope ds(m0->device);
+  if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  hipStream_t stream = (hipStream_t)hip_stream;
+  // two ping-pong buffers of [n_levels][T][B][H] for the intermediate layers
+  size_t hmax = 0;
+  for (int l = 0; l + 1 < n_layers; ++l) hmax = std::max(hmax, (size_t)layers[l]->H);
+  const size_t one = (size_t)n_levels * T * B * hmax;
+  if (2 * one > m0->stack_cap) {
+    HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    dfree(m0->d_stack);
+    m0->stack_cap = 0;
+    HIP_TRY(hipMalloc(&m0->d_stack, 2 * one * sizeof(float)), "hipMalloc(stack)");
+    m0->stack_cap = 2 * one;
+  }
+  // layer 0 runs every level at once (they share x); later layers run each
+  // level on that level's output of the layer below
+  std::vector<int32_t> lv(n_levels);
+  for (int j = 0; j < n_levels; ++j) lv[j] = levels[(size_t)j * n_layers];
+  float* cur = m0->d_stack;
+  approx_lstm_status st = approx_lstm_run(layers[0], x, T, B, nullptr, nullptr, lv.data(), n_levels, cur, nullptr,
+                                          hip_stream);
+  if (st != APPROX_LSTM_OK) return st;
+  for (int l = 1; l < n_layers; ++l) {
+    const bool last = l + 1 == n_layers;
+    float* nxt = last ? h_out : (cur == m0->d_stack ? m0->d_stack + one : m0->d_stack);
+    const size_t in_sz = (size_t)T * B * layers[l - 1]->H, out_sz = (size_t)T * B * layers[l]->H;
+    for (int j = 0; j < n_levels; ++j) {
+      const int32_t K = levels[(size_t)j * n_layers + l];
+      st = approx_lstm_run(layers[l], cur + j * in_sz, T, B, nullptr, nullptr, &K, 1, nxt + j * out_sz, nullptr,
+                           hip_stream);
+      if (st != APPROX_LSTM_OK) return st;
+    }
+    cur = nxt;
+  }
+  return APPROX_LSTM_OK;
+}
+
 approx_lstm_status approx_lstm_check(approx_lstm_model* m, void* hip_stream) {
   g_last_error.clear();
   if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
@@ -439,6 +515,103 @@ approx_lstm_status approx_lstm_set_timing(approx_lstm_model* m, int32_t enable) 
   g_last_error.clear();
   if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
   m->timing = enable ? 1 : 0;
+  return APPROX_LSTM_OK;
+}
+
+namespace {
+
+// Mean in-kernel microseconds per timestep of the last timed run, and the
+// per-timestep values (stamp of one timestep's start to the next one's).
+approx_lstm_status per_step_us(approx_lstm_model* m, void* hip_stream, int T, std::vector<double>& steps, double* mean) {
+  std::vector<double> st(2 + 4 * (size_t)T);
+  approx_lstm_status s = approx_lstm_get_timing(m, hip_stream, st.data(), (int32_t)st.size());
+  if (s != APPROX_LSTM_OK) return s;
+  steps.resize(T);
+  double sum = 0.0;
+  for (int t = 0; t < T; ++t) {
+    const double next = (t + 1 < T) ? st[1 + 4 * (t + 1)] : st[1 + 4 * T];
+    steps[t] = next - st[1 + 4 * t];
+    sum += steps[t];
+  }
+  *mean = T > 0 ? sum / T : 0.0;
+  return APPROX_LSTM_OK;
+}
+
+}  // namespace
+
+approx_lstm_status approx_lstm_run_deadline(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                            const float* h0, const float* c0, double deadline_us_per_step,
+                                            float* h_out, int32_t* k_achieved, float* step_us, void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (!m->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "model has no device store (HOST_ONLY)");
+  if (T < 1 || B < 1 || !x || !h_out || !k_achieved) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
+  if (!(deadline_us_per_step > 0.0)) return fail(APPROX_LSTM_ERR_INVALID_ARG, "deadline must be > 0");
+  const int saved_timing = m->timing;
+  m->timing = 1;
+  auto measure = [&](int K, double* mean, std::vector<double>* steps) -> approx_lstm_status {
+    approx_lstm_status s = approx_lstm_run(m, x, T, B, h0, c0, &K, 1, h_out, nullptr, hip_stream);
+    if (s != APPROX_LSTM_OK) return s;
+    std::vector<double> tmp;
+    s = per_step_us(m, hip_stream, T, steps ? *steps : tmp, mean);
+    if (s != APPROX_LSTM_OK) return s;
+    return approx_lstm_check(m, hip_stream);
+  };
+  approx_lstm_status st = APPROX_LSTM_OK;
+  // calibration: K = 0, 1, 2, 4, ..., rank (cached for this T, B and launch width)
+  if (m->calib_T != T || m->calib_B != B || m->calib_blocks != m->launch_blocks || m->calib.empty()) {
+    m->calib.clear();
+    std::vector<int> ks{0};
+    for (int k = 1; k < m->N; k *= 2) ks.push_back(k);
+    ks.push_back(m->N);
+    for (int k : ks) {
+      double us = 0.0;
+      st = measure(k, &us, nullptr);
+      if (st != APPROX_LSTM_OK) break;
+      m->calib.emplace_back(k, us);
+    }
+    if (st != APPROX_LSTM_OK) {
+      m->calib.clear();
+      m->timing = saved_timing;
+      return st;
+    }
+    m->calib_T = T;
+    m->calib_B = B;
+    m->calib_blocks = m->launch_blocks;
+  }
+  // largest calibrated K within the deadline, then bisection towards the next
+  // calibrated K with fresh measurements
+  int lo = -1, hi = -1;
+  for (size_t i = 0; i < m->calib.size(); ++i) {
+    if (m->calib[i].second <= deadline_us_per_step) {
+      lo = m->calib[i].first;
+      hi = (i + 1 < m->calib.size()) ? m->calib[i + 1].first : lo;
+    }
+  }
+  if (lo < 0) {
+    m->timing = saved_timing;
+    return fail(APPROX_LSTM_ERR_DEADLINE_INFEASIBLE, "K = 0 takes %.3f us per timestep, above %.3f",
+                m->calib[0].second, deadline_us_per_step);
+  }
+  while (hi - lo > 1) {
+    const int mid = lo + (hi - lo) / 2;
+    double us = 0.0;
+    st = measure(mid, &us, nullptr);
+    if (st != APPROX_LSTM_OK) {
+      m->timing = saved_timing;
+      return st;
+    }
+    if (us <= deadline_us_per_step) lo = mid; else hi = mid;
+  }
+  std::vector<double> steps;
+  double mean = 0.0;
+  st = measure(lo, &mean, &steps);
+  m->timing = saved_timing;
+  if (st != APPROX_LSTM_OK) return st;
+  for (int t = 0; t < T; ++t) {
+    k_achieved[t] = lo;
+    if (step_us) step_us[t] = (float)steps[t];
+  }
   return APPROX_LSTM_OK;
 }
 

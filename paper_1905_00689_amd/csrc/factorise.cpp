@@ -161,7 +161,7 @@ double tri_top_eigen(const double* a, const double* b, int m, std::vector<double
 }  // namespace
 
 double lanczos_top(const double* G, int n, double tol, int max_iter, double* y, bool* converged,
-                   int* iterations) {
+                   int* iterations, int threads) {
   const int kmax = (max_iter > 0) ? std::min(max_iter, n) : n;
   std::vector<double> Q((size_t)(kmax + 1) * n), w(n), c(kmax + 1), alpha, beta, s;
   start_vector(Q.data(), n);
@@ -174,7 +174,9 @@ double lanczos_top(const double* G, int n, double tol, int max_iter, double* y, 
   bool done = false;
   for (int k = 0; k < kmax && !done; ++k) {
     const double* q = &Q[(size_t)k * n];
-    for (int i = 0; i < n; ++i) w[i] = dot(G + (size_t)i * n, q, n);
+    double* wp = w.data();
+#pragma omp parallel for num_threads(threads) schedule(static) if (threads > 1 && n >= 256)
+    for (int i = 0; i < n; ++i) wp[i] = dot(G + (size_t)i * n, q, n);
     double al = dot(q, w.data(), n);
     axpy(-al, q, w.data(), n);
     if (k > 0) axpy(-beta[k - 1], &Q[(size_t)(k - 1) * n], w.data(), n);
@@ -209,8 +211,10 @@ double lanczos_top(const double* G, int n, double tol, int max_iter, double* y, 
 
 namespace {
 
-void gram_exact(const std::vector<double>& R, int rows, int cols, bool left, std::vector<double>& G) {
+void gram_exact(const std::vector<double>& R, int rows, int cols, bool left, std::vector<double>& G, int threads) {
   if (left) {
+    // row i of the upper triangle, rows dealt cyclically to balance the triangle
+#pragma omp parallel for num_threads(threads) schedule(static, 1) if (threads > 1)
     for (int i = 0; i < rows; ++i)
       for (int j = i; j < rows; ++j) {
         double v = dot(&R[(size_t)i * cols], &R[(size_t)j * cols], cols);
@@ -255,16 +259,16 @@ int factorise_group(const double* W, int rows, int cols, int rank, int nz,
   const bool left = rows <= cols;
   const int n = left ? rows : cols;
   std::vector<double> G((size_t)n * n);
-  gram_exact(R, rows, cols, left, G);
+  gram_exact(R, rows, cols, left, G, opt.threads);
 
   std::vector<double> y(n), uu(rows), vv(cols), w(left ? rows : cols);
   std::vector<int32_t> idx(cols);
   double tau = 0.0;
   for (int t = 0; t < rank; ++t) {
-    if (t > 0 && opt.gram_refresh > 0 && t % opt.gram_refresh == 0) gram_exact(R, rows, cols, left, G);
+    if (t > 0 && opt.gram_refresh > 0 && t % opt.gram_refresh == 0) gram_exact(R, rows, cols, left, G, opt.threads);
     bool conv = false;
     int iters = 0;
-    lanczos_top(G.data(), n, opt.lanczos_tol, opt.max_lanczos, y.data(), &conv, &iters);
+    lanczos_top(G.data(), n, opt.lanczos_tol, opt.max_lanczos, y.data(), &conv, &iters, opt.threads);
     double s;
     if (left) {
       uu.assign(y.begin(), y.end());

@@ -21,7 +21,8 @@ struct GroupFactors {
 
 struct FactoriseOptions {
   bool keep_unpruned = false;
-  int gram_refresh = 8;         // recompute the Gram matrix exactly every this many steps
+  int gram_refresh = 32;        // recompute the Gram matrix exactly every this many steps
+  int threads = 1;              // threads for the row loops of one group (results do not depend on it)
   double lanczos_tol = 4e-14;   // Ritz residual / Ritz value at which a solve stops
   double stop_rel = 1e-12;      // sigma <= stop_rel * sigma_1 ends the term list
   int max_lanczos = 0;          // 0: up to the Gram size
@@ -38,6 +39,6 @@ int factorise_group(const double* W, int rows, int cols, int rank, int nz,
 // eigenvector to y and returns the eigenvalue; *converged tells whether the
 // Ritz residual met tol (relative to the eigenvalue).
 double lanczos_top(const double* G, int n, double tol, int max_iter, double* y, bool* converged,
-                   int* iterations);
+                   int* iterations, int threads = 1);
 
 }  // namespace alstm

@@ -240,7 +240,8 @@ __host__ __device__ inline Layout layout_of(const RunArgs& a) {
   const size_t LB = (size_t)a.L * a.B;
   const size_t kmax = a.G > 0 ? (size_t)a.GK / a.G : 0;
   size_t o = 0;
-  l.zs = o;     o = align16(o + 4 * (a.GK > 1 ? (size_t)a.GK : 1));   // z of one (level, seq), [g][Kmax]
+  // z of one (level, seq), [g][Kmax]; a single workgroup keeps every pair's
+  l.zs = o;     o = align16(o + 4 * (a.P == 1 ? LB : 1) * (a.GK > 1 ? (size_t)a.GK : 1));
   l.hs = o;     o = align16(o + 4 * LB * a.H);                        // h_{t-1} per (level, seq)
   l.ys = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // y of the owned rows
   l.bs = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // bias of the owned rows
@@ -393,8 +394,8 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
   }
   __syncthreads();
 
-  // A single workgroup running a single recurrence keeps z and h in LDS.
-  const bool local = (P == 1 && LB == 1);
+  // A single workgroup keeps z and h in LDS: nothing is exchanged.
+  const bool local = (P == 1);
   // The last wave does every global store of the recurrence (exchange words
   // and h_out); the other waves do the gathers, so no wave waits on its own
   // stores before its loads.
@@ -430,7 +431,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           if (sla == 0 && ia < nl) {
             const float z = sig[ia] * (pxc[b * OM + ia] + acc);
             const int tau = j + ia * P;
-            if (local) zs[(tau % G) * Kmax + tau / G] = z;
+            if (local) zs[lb * GK + (tau % G) * Kmax + tau / G] = z;
             else zown[lb * OM + ia] = z;
           }
         }
@@ -448,7 +449,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           if (sla == 0 && i < nl) {
             const float z = sig[i] * (pxc[b * OM + i] + acc);
             const int tau = j + i * P;
-            if (local) zs[(tau % G) * Kmax + tau / G] = z;
+            if (local) zs[lb * GK + (tau % G) * Kmax + tau / G] = z;
             else zown[lb * OM + i] = z;
           }
         }
@@ -487,6 +488,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
         }
         lds_barrier();
         if (stamp && lb == 0) a.stamps[4 + 4 * t] = clock64();
+        const float* zl = zs + (local ? lb * GK : 0);
         if constexpr (UPT > 0) {
           // branch-free: entries past the budget multiply a valid z by 0
 #pragma unroll
@@ -496,7 +498,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
 #pragma unroll
             for (int k = 0; k < UPT; ++k) {
               const int n = slb + S0 * k;
-              zv[k] = zs[zbase[o] + (n < Kl ? n : 0)];
+              zv[k] = zl[zbase[o] + (n < Kl ? n : 0)];
             }
             float acc = 0.0f;
 #pragma unroll
@@ -516,7 +518,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
             if (ol < outs) {
               q = ol / rc;
               rr = ol - q * rc;
-              const float* zg = zs + ((G == 4) ? q : 0) * Kmax;
+              const float* zg = zl + ((G == 4) ? q : 0) * Kmax;
               if (a.ustride) {
                 const float* urow = us + (size_t)(q * RP + rr) * a.ustride;
 #pragma unroll 8
@@ -541,7 +543,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           const float hv2 = go * tanh_fast(c);
           cs[lb * RP + rr] = c;
           hown[lb * RP + rr] = hv2;
-          if (local) hs[r0 + rr] = hv2;
+          if (local) hs[lb * H + r0 + rr] = hv2;
         }
         lds_barrier();
       }
@@ -764,10 +766,14 @@ size_t plan_progressive(RunArgs& a, int P) {
     const int need_u = (Kmax + S - 1) / S;
     const int need_o = (4 * a.rows_per * S + kThreads - 1) / kThreads;
     if (need_o <= 1 && need_u <= 32) { a.opt = 1; a.upt = 32; }
+    else if (need_o <= 1 && need_u <= 64) { a.opt = 1; a.upt = 64; }
     else if (need_o <= 2 && need_u <= 16) { a.opt = 2; a.upt = 16; }
     else if (need_o <= 4 && need_u <= 8) { a.opt = 4; a.upt = 8; }
     if (a.opt == 1 && need_u <= 8) a.upt = 8;
     else if (a.opt == 1 && need_u <= 16) a.upt = 16;
+    // 64 U entries per thread only next to at most 12 h-part entries per
+    // lane: beyond that the register file (256 per lane) spills
+    if (a.upt == 64 && a.hpl > 12) { a.opt = 0; a.upt = 0; }
   }
   a.P = P;
   a.vh_lds = 0;
@@ -812,6 +818,8 @@ hipError_t launch_u(const RunArgs& a, int blocks, int cooperative, size_t lds, h
   if (a.opt == 1 && a.upt == 8) return launch_one<HPL, 1, 8>(a, blocks, cooperative, lds, stream);
   if (a.opt == 1 && a.upt == 16) return launch_one<HPL, 1, 16>(a, blocks, cooperative, lds, stream);
   if (a.opt == 1 && a.upt == 32) return launch_one<HPL, 1, 32>(a, blocks, cooperative, lds, stream);
+  if constexpr (HPL <= 12)
+    if (a.opt == 1 && a.upt == 64) return launch_one<HPL, 1, 64>(a, blocks, cooperative, lds, stream);
   if (a.opt == 2) return launch_one<HPL, 2, 16>(a, blocks, cooperative, lds, stream);
   if (a.opt == 4) return launch_one<HPL, 4, 8>(a, blocks, cooperative, lds, stream);
   return launch_one<HPL, 1, 0>(a, blocks, cooperative, lds, stream);

@@ -196,3 +196,109 @@ def test_driving_full_rank_without_pruning_is_the_exact_lstm(driving):
     h, _ = run_gpu(m, driving.x, [512])
     he, _ = oracle.exact_lstm(driving.W, driving.b, driving.x)
     assert rel_err(h[0], he) < TOL
+
+
+# ----------------------------------------------------------------- stack
+def oracle_stack(factors, biases, x, levels):
+    """Layer-by-layer oracle: layer l at level j reads layer l-1's h at level j."""
+    out = []
+    for lv in levels:
+        inp = x
+        for f, b, K in zip(factors, biases, lv):
+            hs, _ = oracle.run(f, b, inp, [K])
+            inp = hs[0]
+        out.append(inp)
+    return np.stack(out)
+
+
+@pytest.mark.parametrize("independent", [True, False])
+def test_stack_matches_layerwise_oracle(independent):
+    """Two stacked layers (the stacked workload at a quarter of its sizes:
+    D=1024 -> H=256 -> H=256, T=8, 75% pruning).  Per-layer budgets; with
+    independent=True the oracle prepares its own factors (K inside the chain
+    agreement horizon), else it runs on the library's exported terms."""
+    w = synth.make(1024, 256, 8, 1, index=14, xkind="relu", n_layers=2)
+    (W1, b1), (W2, b2) = w.layers
+    levels = [(8, 8), (16, 4)] if independent else [(16, 16), (64, 64), (256, 256), (0, 256), (256, 0)]
+    rank = 16 if independent else 256
+    say("stack 1024->256->256 levels", levels, "independent", independent)
+    m1 = B.approx_lstm_prepare(W1[:, :1024], W1[:, 1024:], b1, 1024, 256, rank, prune_ratio=0.75)
+    m2 = B.approx_lstm_prepare(W2[:, :256], W2[:, 256:], b2, 256, 256, rank, prune_ratio=0.75)
+    if independent:
+        f1 = oracle.prepare(W1, 256, rank, oracle.nz_from_ratio(1280, 0.75))
+        f2 = oracle.prepare(W2, 256, rank, oracle.nz_from_ratio(512, 0.75))
+    else:
+        f1, f2 = exported_factors(m1), exported_factors(m2)
+    xt = torch.from_numpy(w.x).cuda()
+    h = torch.full((len(levels), 8, 1, 256), float("nan"), device="cuda")
+    B.approx_lstm_run_stack([m1, m2], xt, levels, h)
+    B.approx_lstm_check(m1)
+    B.approx_lstm_check(m2)
+    torch.cuda.synchronize()
+    ho = oracle_stack([f1, f2], [b1, b2], w.x, levels)
+    hg = h.cpu().numpy()
+    for j, lv in enumerate(levels):
+        assert rel_err(hg[j], ho[j]) < TOL, (lv, rel_err(hg[j], ho[j]))
+
+
+def test_stack_rejects_mismatched_layers():
+    w = synth.named("tiny")
+    m1 = prep(w, 4, 0.5)                   # D=64, H=32
+    m2 = prep(w, 4, 0.5)                   # expects input 64, gets 32
+    xt = torch.zeros((2, 1, 64), device="cuda")
+    h = torch.zeros((1, 2, 1, 32), device="cuda")
+    with pytest.raises(B.ApproxLstmError) as ei:
+        B.approx_lstm_run_stack([m1, m2], xt, [(1, 1)], h)
+    assert ei.value.status == B.ERR_INVALID_ARG
+
+
+# -------------------------------------------------------------- deadline
+@pytest.fixture(scope="module")
+def deadline_small():
+    """The deadline workload at a quarter of its sizes: D=512 -> H=512, T=16,
+    batch 2, rank 512, 90% pruning."""
+    w = synth.make(512, 512, 16, 2, index=15, xkind="relu")
+    say("prepare deadline-shaped D=512 H=512 rank 512 p=0.9")
+    m = B.approx_lstm_prepare(w.W[:, :512], w.W[:, 512:], w.b, 512, 512, 512, prune_ratio=0.9)
+    return w, m
+
+
+def test_deadline_mode_picks_budget_and_matches_replay(deadline_small):
+    """A generous deadline buys every term; tighter deadlines (fractions of
+    the full-rank step time) buy no more terms; every output equals the
+    progressive LSTM replayed at the achieved budgets."""
+    w, m = deadline_small
+    f = exported_factors(m)
+    xt = torch.from_numpy(w.x).cuda()
+    he, _ = oracle.exact_lstm(w.W, w.b, w.x)
+    ks, full_us = [], None
+    for frac in (None, 0.8, 0.6):
+        dl = 1e6 if frac is None else frac * full_us
+        say("deadline", dl, "us/step")
+        h = torch.full((16, 2, 512), float("nan"), device="cuda")
+        try:
+            k, us = B.approx_lstm_run_deadline(m, xt, dl, h)
+        except B.ApproxLstmError as e:
+            assert e.status == B.ERR_DEADLINE_INFEASIBLE and frac is not None
+            say("  infeasible:", str(e))
+            continue
+        torch.cuda.synchronize()
+        if frac is None:
+            full_us = float(np.median(us))
+        assert np.all(k == k[0]) and 0 <= k[0] <= 512
+        ks.append(int(k[0]))
+        ho, _ = oracle.run_schedule(f, w.b, w.x, list(k))
+        assert rel_err(h.cpu().numpy(), ho) < TOL, dl
+        say("  K", k[0], "median step us", float(np.median(us)), "max |h - exact|",
+            float(np.abs(h.cpu().numpy() - he).max()))
+    assert ks[0] == 512
+    assert all(a >= b for a, b in zip(ks, ks[1:]))
+
+
+def test_deadline_infeasible(deadline_small):
+    w, m = deadline_small
+    xt = torch.from_numpy(w.x).cuda()
+    h = torch.zeros((16, 2, 512), device="cuda")
+    with pytest.raises(B.ApproxLstmError) as ei:
+        B.approx_lstm_run_deadline(m, xt, 1e-3, h)
+    assert ei.value.status == B.ERR_DEADLINE_INFEASIBLE
