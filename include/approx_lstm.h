@@ -71,7 +71,9 @@ typedef struct {
   double prune_ratio;   /* p in [0, 1); used only when nz == 0 */
   int32_t groups;       /* 4: each gate's H x C block is factorised separately (the paper's scheme);
                            1: the stacked 4H x C matrix is factorised as one */
-  int32_t factor_dtype; /* 0 = fp32 factors (the only value this build accepts) */
+  int32_t factor_dtype; /* 0 = fp32 factors (sparse store, persistent run kernel);
+                           1 = bf16 factor values stored as dense zero-filled panels, run by
+                           MFMA kernels with fp32 accumulation (for many sequences at once) */
   uint64_t flags;       /* APPROX_LSTM_FLAG_* */
 } approx_lstm_prepare_params;
 
@@ -83,6 +85,7 @@ typedef struct {
   int32_t unconverged_steps;                  /* solves that missed tolerance (0 normally) */
   int32_t has_device_store;
   uint64_t device_bytes;                      /* factor store on the device */
+  int32_t factor_dtype;                       /* as prepared */
 } approx_lstm_info;
 
 /*
@@ -102,7 +105,9 @@ typedef struct {
  * positive; mask = the NZ entries of largest |v| (ties to the lower index),
  * ascending; R <- R - sigma u prune(v)^T.  A step with sigma <= 1e-12 times
  * the first step's sigma ends the list: that and every later term are zero.
- * Values are then rounded to fp32 (nearest even).  Synchronises hip_stream
+ * Values are then rounded to fp32 (nearest even); with factor_dtype 1, u and
+ * the v values are further rounded fp32 -> bf16 (nearest even) while sigma
+ * stays fp32; masks are decided in fp64 before any rounding.  Synchronises hip_stream
  * before returning.  Returns NOT_CONVERGED (with a usable model) if a solve
  * missed its tolerance.
  */
@@ -124,7 +129,11 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
  *   c_out    device [n_levels][B][H] or NULL: final cell state of each level
  *
  * Each level is its own recurrence (its h feeds only itself); the x-part of
- * the projections is shared.  Asynchronous on hip_stream; the call blocks
+ * the projections is shared.  With a bf16 model (factor_dtype 1) every
+ * product takes bf16 operands -- x~ = [x_t; h_{t-1}], the factor values and
+ * z = sigma * (prune(v)^T x~) -- with fp32 accumulation; h_out and c_out stay
+ * fp32; sequences are padded to a multiple of 64 internally (B <= 2^20 and
+ * T * padded B <= 2^30, else UNSUPPORTED).  Asynchronous on hip_stream; the call blocks
  * only to allocate workspace on first use (see approx_lstm_reserve).  The
  * device-side waits of the kernel are bounded; if one expires the next
  * approx_lstm_check call reports APPROX_LSTM_ERR_DEVICE.
@@ -146,6 +155,7 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
  *   k_achieved       host [T]: the K used at every timestep
  *   step_us          host [T] or NULL: measured microseconds of every timestep
  *
+ * fp32 models only (UNSUPPORTED for factor_dtype 1).
  * On first use for a (T, B, launch width) the call calibrates time against K
  * by running the sequence at K = 0, 1, 2, 4, ..., rank (cached in the model),
  * then bisects between the two calibrated budgets around the deadline with
@@ -224,7 +234,8 @@ approx_lstm_status approx_lstm_model_info(const approx_lstm_model* m, approx_lst
 
 /*
  * approx_lstm_get_factors -- copy group g's refinement terms, in refinement
- * order, as the device store holds them (fp32), to host arrays:
+ * order, as the device store holds them (fp32; for a bf16 model the fp32
+ * values are exactly the stored bf16 values), to host arrays:
  *   sigma [rank], u [rank][R_g], v_idx [rank][nz] (ascending column indices
  *   into [x; h], 0..C-1), v_val [rank][nz] (entries of prune(v) on v_idx).
  * Any output pointer may be NULL.  Reads the host copy kept by prepare.

@@ -41,8 +41,10 @@ def run_schedule(f, b, x, Ks, h0=None, c0=None, operand_round=None):
     """One recurrence with budget Ks[t] at timestep t.
 
     f: Factors; b: [4H] or None; x: [T, B, D].  Returns (h [T, B, H], c_T [B, H]).
-    operand_round='bf16' rounds x~ to bf16 before the products (the batched
-    bf16 path multiplies bf16 operands with fp32 accumulation).
+    operand_round='bf16' gives both products bf16 operands, as the batched
+    bf16 configuration computes them (bf16 operands, fp32 accumulation):
+    x~ is rounded before prune(v)^T x~, and z = sigma * s before the
+    accumulation into the gates (the factor values come rounded in f).
     """
     x = np.asarray(x, dtype=np.float64)
     T, B, D = x.shape
@@ -64,6 +66,8 @@ def run_schedule(f, b, x, Ks, h0=None, c0=None, operand_round=None):
                 continue
             s = Vd[g][:n] @ xt.T                          # prune(v_n)^T x~   [n, B]
             z = f.sigma[g, :n, None] * s                  # sigma_n * s_n
+            if operand_round == "bf16":
+                z = round_bf16(z)
             y[:, g * Rg:(g + 1) * Rg] += (f.U[g, :n].T @ z).T   # sum_n z_n u_n
         y += bias
         h, c = cell_update(y, c)

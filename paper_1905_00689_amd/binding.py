@@ -46,7 +46,7 @@ class Info(ctypes.Structure):
                 ("rows_per_group", ctypes.c_int32), ("rank", ctypes.c_int32),
                 ("nz", ctypes.c_int32), ("eff_rank", ctypes.c_int32 * 4),
                 ("unconverged_steps", ctypes.c_int32), ("has_device_store", ctypes.c_int32),
-                ("device_bytes", ctypes.c_uint64)]
+                ("device_bytes", ctypes.c_uint64), ("factor_dtype", ctypes.c_int32)]
 
 
 if not os.path.exists(LIB_PATH):

@@ -84,6 +84,18 @@ struct approx_lstm_model {
   uint16_t* d_nx = nullptr;
   uint64_t dev_bytes = 0;
   int num_cu = 0;
+  // bf16 panel store (factor_dtype 1): Vx [prow][Dp], Vh [prow][Hp], Ut [4H][Kp]
+  int dtype = 0;
+  int Dp = 0, Hp = 0, Kp = 0, prow = 0;
+  uint16_t* d_Vx = nullptr;
+  uint16_t* d_Vh = nullptr;
+  uint16_t* d_Ut16 = nullptr;
+  uint16_t* d_bz = nullptr;          // batched workspace: Z [G][Bp][Kp]
+  size_t bz_cap = 0;
+  uint16_t* d_bh = nullptr;          // hb [Bp][Hp]
+  size_t bh_cap = 0;
+  float* d_bc = nullptr;             // c [Bp][H]
+  size_t bc_cap = 0;
   std::vector<int> hpre;             // [N*G] max over terms 0..tau of the h-part entry count
   // run workspace
   float* d_px = nullptr;
@@ -108,8 +120,14 @@ struct approx_lstm_model {
   int cooperative = 0;               // 1: cooperative launch API
 
   ~approx_lstm_model() {
-    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err && !d_stamps && !d_stack) return;
+    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err && !d_stamps && !d_stack && !d_bz && !d_bh && !d_bc) return;
     DeviceScope ds(device);
+    dfree(d_Vx);
+    dfree(d_Vh);
+    dfree(d_Ut16);
+    dfree(d_bz);
+    dfree(d_bh);
+    dfree(d_bc);
     dfree(d_sigma);
     dfree(d_Ut);
     dfree(d_vval);
@@ -166,6 +184,71 @@ approx_lstm_status ensure_workspace(approx_lstm_model* m, size_t px_floats, size
   return APPROX_LSTM_OK;
 }
 
+// fp64 -> fp32 (nearest even) -> bf16 (nearest even), returned as the fp32
+// value it represents; finite inputs.
+float round_bf16(double v) {
+  float f = (float)v;
+  uint32_t bits;
+  std::memcpy(&bits, &f, 4);
+  bits = (bits + 0x7FFFu + ((bits >> 16) & 1u)) & 0xFFFF0000u;
+  std::memcpy(&f, &bits, 4);
+  return f;
+}
+
+uint16_t bf16_bits_of(float exact_bf16) {
+  uint32_t bits;
+  std::memcpy(&bits, &exact_bf16, 4);
+  return (uint16_t)(bits >> 16);
+}
+
+size_t round_up(size_t v, size_t m) { return (v + m - 1) / m * m; }
+
+template <class T>
+approx_lstm_status grow(T*& p, size_t& cap, size_t want, hipStream_t stream, const char* what) {
+  if (want <= cap) return APPROX_LSTM_OK;
+  HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+  dfree(p);
+  cap = 0;
+  HIP_TRY(hipMalloc(&p, want * sizeof(T)), what);
+  cap = want;
+  return APPROX_LSTM_OK;
+}
+
+// Workspace of the batched path for T timesteps, Bp padded sequences and
+// budgets up to kmax.
+approx_lstm_status ensure_batched(approx_lstm_model* m, int T, size_t Bp, int kmax, hipStream_t stream) {
+  const size_t prows = (size_t)m->G * round_up((size_t)kmax, 32);
+  approx_lstm_status st = grow(m->d_px, m->px_cap, std::max<size_t>(1, prows * T * Bp), stream, "hipMalloc(P)");
+  if (st == APPROX_LSTM_OK) st = grow(m->d_bz, m->bz_cap, (size_t)m->G * Bp * m->Kp, stream, "hipMalloc(Z)");
+  if (st == APPROX_LSTM_OK) st = grow(m->d_bh, m->bh_cap, Bp * m->Hp, stream, "hipMalloc(hb)");
+  if (st == APPROX_LSTM_OK) st = grow(m->d_bc, m->bc_cap, Bp * m->H, stream, "hipMalloc(c)");
+  return st;
+}
+
+// The batched bf16 run (factor_dtype 1): arguments already checked.
+approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int B, const float* h0, const float* c0,
+                               const int32_t* levels, int n_levels, float* h_out, float* c_out,
+                               hipStream_t stream) {
+  const size_t Bp = round_up((size_t)B, 64);
+  if (Bp > ((size_t)1 << 20)) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "B = %d exceeds 2^20 for a bf16 model", B);
+  if ((size_t)T * Bp > (size_t)1 << 30)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T * padded B = %zu exceeds 2^30", (size_t)T * Bp);
+  int kmax = 0;
+  for (int l = 0; l < n_levels; ++l) kmax = std::max(kmax, (int)levels[l]);
+  approx_lstm_status st = ensure_batched(m, T, Bp, kmax, stream);
+  if (st != APPROX_LSTM_OK) return st;
+  alstm::BatchedArgs a{};
+  a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
+  a.sigma = m->d_sigma; a.Vx = m->d_Vx; a.Vh = m->d_Vh; a.Ut = m->d_Ut16; a.bias = m->d_bias;
+  a.P = m->d_px; a.Z = m->d_bz; a.hb = m->d_bh; a.c = m->d_bc;
+  a.D = m->D; a.Dp = m->Dp; a.H = m->H; a.Hp = m->Hp; a.G = m->G; a.Kp = m->Kp;
+  a.T = T; a.B = B; a.Bp = (int)Bp;
+  a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
+  std::vector<int> lv(levels, levels + n_levels);
+  HIP_TRY(alstm::launch_batched(a, lv.data(), n_levels, stream), "launch batched kernels");
+  return APPROX_LSTM_OK;
+}
+
 // Workgroups for a run: about one per 32 terms in use (so that every
 // workgroup's terms and rows fit registers), at most 256.
 int auto_blocks(const approx_lstm_model* m, int GK) {
@@ -192,7 +275,8 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
   const int C = (int)Cll;
   if (p->groups != 1 && p->groups != 4) return fail(APPROX_LSTM_ERR_INVALID_ARG, "groups must be 1 or 4");
   if (p->rank < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "rank must be >= 1");
-  if (p->factor_dtype != 0) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "only fp32 factors (factor_dtype 0) are built");
+  if (p->factor_dtype != 0 && p->factor_dtype != 1)
+    return fail(APPROX_LSTM_ERR_INVALID_ARG, "factor_dtype must be 0 (fp32) or 1 (bf16)");
   int nz = p->nz;
   if (nz == 0) {
     if (!(p->prune_ratio >= 0.0 && p->prune_ratio < 1.0))
@@ -207,6 +291,7 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
   if (!m) return fail(APPROX_LSTM_ERR_OUT_OF_MEMORY, "host allocation failed");
   const int G = p->groups, Rg = 4 * H / G, N = p->rank;
   m->D = D; m->H = H; m->C = C; m->G = G; m->Rg = Rg; m->N = N; m->NZ = nz; m->flags = p->flags;
+  m->dtype = p->factor_dtype;
 
   std::vector<alstm::GroupFactors> gf(G);
   try {
@@ -237,15 +322,19 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
       m->u64.assign((size_t)G * N * Rg, 0.0);
       m->v64.assign((size_t)G * N * C, 0.0);
     }
+    // stored values: fp32 (nearest even), or bf16 via fp32; sigma is fp32 in
+    // both, and the masks were decided in fp64 before any rounding
+    const bool bf = m->dtype == 1;
+    auto store = [bf](double v) { return bf ? round_bf16(v) : (float)v; };
     for (int g = 0; g < G; ++g) {
       m->eff_rank[g] = gf[g].eff_rank;
       m->unconverged += gf[g].unconverged;
       for (int n = 0; n < N; ++n) {
         m->sigma[(size_t)g * N + n] = (float)gf[g].sigma[n];
-        for (int r = 0; r < Rg; ++r) m->u[((size_t)g * N + n) * Rg + r] = (float)gf[g].u[(size_t)n * Rg + r];
+        for (int r = 0; r < Rg; ++r) m->u[((size_t)g * N + n) * Rg + r] = store(gf[g].u[(size_t)n * Rg + r]);
         for (int e = 0; e < nz; ++e) {
           m->vidx[((size_t)g * N + n) * nz + e] = gf[g].mask[(size_t)n * nz + e];
-          m->vval[((size_t)g * N + n) * nz + e] = (float)gf[g].vals[(size_t)n * nz + e];
+          m->vval[((size_t)g * N + n) * nz + e] = store(gf[g].vals[(size_t)n * nz + e]);
         }
       }
       if (keep) {
@@ -289,6 +378,28 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
       const int g = o / Rg, r = o % Rg;
       for (int n = 0; n < N; ++n) Ut_h[(size_t)o * N + n] = m->u[((size_t)g * N + n) * Rg + r];
     }
+    // bf16 models: dense zero-filled panels (x-part and h-part of every v,
+    // U with the term index contiguous), padded for the MFMA tiles
+    std::vector<uint16_t> vx16, vh16, ut16;
+    const bool bf = m->dtype == 1;
+    if (bf) {
+      m->Dp = (int)round_up(D, 32);
+      m->Hp = (int)round_up(H, 32);
+      m->Kp = (int)round_up(N, 32);
+      m->prow = (int)round_up((size_t)G * m->Kp, 64);
+      vx16.assign((size_t)m->prow * m->Dp, 0);
+      vh16.assign((size_t)m->prow * m->Hp, 0);
+      ut16.assign((size_t)4 * H * m->Kp, 0);
+      for (size_t tau = 0; tau < NT; ++tau)
+        for (int e = 0; e < nz; ++e) {
+          const int k = vi_h[tau * nz + e];
+          const uint16_t bits = bf16_bits_of(vv_h[tau * nz + e]);
+          if (k < D) vx16[tau * m->Dp + k] = bits;
+          else vh16[tau * m->Hp + (k - D)] = bits;
+        }
+      for (int o = 0; o < 4 * H; ++o)
+        for (int n = 0; n < N; ++n) ut16[(size_t)o * m->Kp + n] = bf16_bits_of(Ut_h[(size_t)o * N + n]);
+    }
     approx_lstm_status st = APPROX_LSTM_OK;
     auto step = [&](hipError_t e, const char* what) {
       if (st == APPROX_LSTM_OK && e != hipSuccess) st = hip_fail(e, what);
@@ -301,27 +412,28 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
       m->num_cu = prop.multiProcessorCount;
     }
     m->has_dev = true;
-    step(hipMalloc(&m->d_sigma, NT * 4), "hipMalloc(sigma)");
-    step(hipMalloc(&m->d_Ut, Ut_h.size() * 4), "hipMalloc(Ut)");
-    step(hipMalloc(&m->d_vval, vv_h.size() * 4), "hipMalloc(vval)");
-    step(hipMalloc(&m->d_vidx, vi_h.size() * 2), "hipMalloc(vidx)");
-    step(hipMalloc(&m->d_nx, NT * 2), "hipMalloc(nx)");
-    step(hipMalloc(&m->d_bias, (size_t)4 * H * 4), "hipMalloc(bias)");
-    if (st == APPROX_LSTM_OK) {
-      step(hipMemcpyAsync(m->d_sigma, s_h.data(), NT * 4, hipMemcpyHostToDevice, stream), "upload sigma");
-      step(hipMemcpyAsync(m->d_Ut, Ut_h.data(), Ut_h.size() * 4, hipMemcpyHostToDevice, stream), "upload Ut");
-      step(hipMemcpyAsync(m->d_vval, vv_h.data(), vv_h.size() * 4, hipMemcpyHostToDevice, stream), "upload vval");
-      step(hipMemcpyAsync(m->d_vidx, vi_h.data(), vi_h.size() * 2, hipMemcpyHostToDevice, stream), "upload vidx");
-      step(hipMemcpyAsync(m->d_nx, nx_h.data(), NT * 2, hipMemcpyHostToDevice, stream), "upload nx");
-      step(hipMemcpyAsync(m->d_bias, m->bias.data(), (size_t)4 * H * 4, hipMemcpyHostToDevice, stream),
-           "upload bias");
-      step(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    auto up = [&](auto*& dst, const void* src, size_t bytes, const char* what) {
+      step(hipMalloc(&dst, bytes), what);
+      if (st == APPROX_LSTM_OK) step(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream), what);
+      m->dev_bytes += bytes;
+    };
+    up(m->d_sigma, s_h.data(), NT * 4, "sigma");
+    up(m->d_bias, m->bias.data(), (size_t)4 * H * 4, "bias");
+    if (bf) {
+      up(m->d_Vx, vx16.data(), vx16.size() * 2, "Vx panel");
+      up(m->d_Vh, vh16.data(), vh16.size() * 2, "Vh panel");
+      up(m->d_Ut16, ut16.data(), ut16.size() * 2, "U panel");
+    } else {
+      up(m->d_Ut, Ut_h.data(), Ut_h.size() * 4, "Ut");
+      up(m->d_vval, vv_h.data(), vv_h.size() * 4, "vval");
+      up(m->d_vidx, vi_h.data(), vi_h.size() * 2, "vidx");
+      up(m->d_nx, nx_h.data(), NT * 2, "nx");
     }
+    if (st == APPROX_LSTM_OK) step(hipStreamSynchronize(stream), "hipStreamSynchronize");
     if (st != APPROX_LSTM_OK) {
       delete m;
       return st;
     }
-    m->dev_bytes = NT * 4 + Ut_h.size() * 4 + vv_h.size() * 4 + vi_h.size() * 2 + NT * 2 + (size_t)4 * H * 4;
   }
   *out = m;
   if (m->unconverged)
@@ -337,9 +449,16 @@ approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int3
     return fail(APPROX_LSTM_ERR_INVALID_ARG, "reserve sizes out of range");
   DeviceScope ds(m->device);
   if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  approx_lstm_status st;
+  if (m->dtype == 1) {
+    st = ensure_batched(m, T_max, round_up((size_t)B_max, 64), m->N, nullptr);
+    if (st != APPROX_LSTM_OK) return st;
+    HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
+    return APPROX_LSTM_OK;
+  }
   const size_t GK = (size_t)m->G * m->N, LB = (size_t)L_max * B_max;
   const size_t P_max = std::max(1, m->num_cu);
-  approx_lstm_status st = ensure_workspace(m, GK * T_max * B_max, LB * (GK + P_max), LB * m->H, nullptr);
+  st = ensure_workspace(m, GK * T_max * B_max, LB * (GK + P_max), LB * m->H, nullptr);
   if (st != APPROX_LSTM_OK) return st;
   HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
   return APPROX_LSTM_OK;
@@ -368,6 +487,7 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   DeviceScope ds(m->device);
   if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
   hipStream_t stream = (hipStream_t)hip_stream;
+  if (m->dtype == 1) return run_batched(m, x, T, B, h0, c0, levels, n_levels, h_out, c_out, stream);
 
   alstm::RunArgs a{};
   a.D = m->D; a.H = m->H; a.G = m->G; a.N = m->N; a.NZ = m->NZ; a.T = T; a.B = B; a.L = n_levels;
@@ -547,6 +667,7 @@ approx_lstm_status approx_lstm_run_deadline(approx_lstm_model* m, const float* x
   if (!m->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "model has no device store (HOST_ONLY)");
   if (T < 1 || B < 1 || !x || !h_out || !k_achieved) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
   if (!(deadline_us_per_step > 0.0)) return fail(APPROX_LSTM_ERR_INVALID_ARG, "deadline must be > 0");
+  if (m->dtype != 0) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "deadline mode needs an fp32 model");
   const int saved_timing = m->timing;
   m->timing = 1;
   auto measure = [&](int K, double* mean, std::vector<double>* steps) -> approx_lstm_status {
@@ -654,6 +775,7 @@ approx_lstm_status approx_lstm_model_info(const approx_lstm_model* m, approx_lst
   out->unconverged_steps = m->unconverged;
   out->has_device_store = m->has_dev ? 1 : 0;
   out->device_bytes = m->dev_bytes;
+  out->factor_dtype = m->dtype;
   return APPROX_LSTM_OK;
 }
 

@@ -83,4 +83,44 @@ hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hip
 // Zero `n` 64-bit words (exchange-buffer reset) with a plain kernel.
 hipError_t launch_clear_u64(unsigned long long* p, size_t n, hipStream_t stream);
 
+// Batched bf16 path (many sequences; the factors as zero-filled bf16 panels
+// and every product on MFMA with fp32 accumulation).  bf16 arrays are raw
+// 16-bit patterns.  Padded sizes: Dp, Hp multiples of 32; Bp a multiple of 64;
+// Kp = rank rounded up to 32; panel rows = G*Kp rounded up to 64.
+//   x      [T][B][D] fp32           h0, c0 [B][H] fp32 or null
+//   h_out  [L][T][B][H]             c_out  [L][B][H] or null
+//   sigma  [N*G] fp32               term tau = n*G + g
+//   Vx     [rows][Dp] bf16          x-part of prune(v) of term tau (zeros off the mask)
+//   Vh     [rows][Hp] bf16          h-part of prune(v) of term tau
+//   Ut     [4H][Kp] bf16            Ut[o][n] = u of term (n, g(o)) at row o within its group
+//   bias   [4H] fp32
+//   P      [rows_used][T*Bp] fp32   x-part projections, column t*Bp + b (workspace)
+//   Z      [G][Bp][Kp] bf16         sigma * s of the current timestep (workspace)
+//   hb     [Bp][Hp] bf16            h of the previous timestep (workspace)
+//   c      [Bp][H] fp32             cell state (workspace)
+struct BatchedArgs {
+  const float* x;
+  const float* h0;
+  const float* c0;
+  float* h_out;
+  float* c_out;
+  const float* sigma;
+  const uint16_t* Vx;
+  const uint16_t* Vh;
+  const uint16_t* Ut;
+  const float* bias;
+  float* P;
+  uint16_t* Z;
+  uint16_t* hb;
+  float* c;
+  int D, Dp, H, Hp, G, Kp, T, B, Bp;
+  int rows;        // panel rows a launch covers (set per launch)
+  int xvec;        // 1: x rows may be read as 16-byte vectors (D % 4 == 0, x 16-byte aligned)
+};
+
+// Launches, on `stream`, the x-projection once and then, for every level,
+// T pairs of per-timestep kernels.  Requires Bp % 64 == 0 and every level
+// K <= Kp.
+hipError_t launch_batched(const BatchedArgs& a, const int* levels, int n_levels, hipStream_t stream);
+
 }  // namespace alstm

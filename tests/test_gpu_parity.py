@@ -10,64 +10,18 @@ test_library_cpu.py) the oracle runs on the library's exported terms, which
 test_library_cpu.py certifies step by step against the oracle.
 """
 
-import sys
-
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from oracle.factorise import Factors
 from paper_1905_00689_amd import synth
 from paper_1905_00689_amd import binding as B
 
+from .gpu_helpers import exported_factors, prep, rel_err, run_gpu, say
+
 pytestmark = pytest.mark.gpu
 TOL = 1e-4
-
-
-def say(*a):
-    print("[case]", *a, flush=True)
-    sys.stdout.flush()
-
-
-def rel_err(h_gpu, h_orc):
-    num = np.abs(h_gpu - h_orc).max(axis=-1)
-    den = np.maximum(np.abs(h_orc).max(axis=-1), 1e-6)
-    return float((num / den).max())
-
-
-def prep(w, rank, p, groups=4, flags=0):
-    D, H = w.D, w.H
-    return B.approx_lstm_prepare(w.W[:, :D], w.W[:, D:], w.b, D, H, rank, prune_ratio=p,
-                                 groups=groups, flags=flags)
-
-
-def run_gpu(m, x, levels, h0=None, c0=None, want_c=False):
-    T, Bn, D = x.shape
-    H = m.info["hidden_size"]
-    dev = torch.device("cuda")
-    xt = torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(dev)
-    h_out = torch.full((len(levels), T, Bn, H), float("nan"), device=dev)
-    c_out = torch.full((len(levels), Bn, H), float("nan"), device=dev) if want_c else None
-    h0t = None if h0 is None else torch.from_numpy(np.ascontiguousarray(h0, np.float32)).to(dev)
-    c0t = None if c0 is None else torch.from_numpy(np.ascontiguousarray(c0, np.float32)).to(dev)
-    B.approx_lstm_run(m, xt, levels, h_out, h0t, c0t, c_out)
-    B.approx_lstm_check(m)
-    torch.cuda.synchronize()
-    return h_out.cpu().numpy(), (c_out.cpu().numpy() if want_c else None)
-
-
-def exported_factors(m):
-    """The library's stored terms as an oracle Factors object (fp32 values)."""
-    inf = m.info
-    G, N, Rg, nz, C = inf["groups"], inf["rank"], inf["rows_per_group"], inf["nz"], inf["aug_size"]
-    sig = np.zeros((G, N)); U = np.zeros((G, N, Rg)); mask = np.zeros((G, N, nz), np.int64)
-    vals = np.zeros((G, N, nz))
-    for g in range(G):
-        f = B.approx_lstm_get_factors(m, g)
-        sig[g], U[g], mask[g], vals[g] = f["sigma"], f["u"], f["v_idx"], f["v_val"]
-    return Factors(inf["input_size"], inf["hidden_size"], G, N, nz, sig, U, mask, vals,
-                   np.zeros((G, N, C)), np.array(inf["eff_rank"]), "f32")
 
 
 # ------------------------------------------------------------------ tiny

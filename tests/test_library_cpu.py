@@ -164,7 +164,7 @@ def test_nz_from_ratio_matches_oracle():
     (dict(nz=97), B.ERR_INVALID_ARG),
     (dict(nz=-1), B.ERR_INVALID_ARG),
     (dict(prune_ratio=1.0), B.ERR_INVALID_ARG),
-    (dict(factor_dtype=1), B.ERR_UNSUPPORTED),
+    (dict(factor_dtype=2), B.ERR_INVALID_ARG),
 ])
 def test_prepare_rejects_bad_arguments(kw, status):
     w = synth.named("tiny")
@@ -174,6 +174,27 @@ def test_prepare_rejects_bad_arguments(kw, status):
         B.approx_lstm_prepare(w.W[:, :64], w.W[:, 64:], w.b, 64, 32, **args)
     assert ei.value.status == status
     assert B.approx_lstm_last_error()
+
+
+@pytest.mark.parametrize("G", [4, 1])
+def test_bf16_model_stores_rounded_values_of_the_same_chain(G):
+    """factor_dtype 1: the masks are those of the fp32 model (decided in fp64
+    before rounding), sigma stays fp32, and u and the v values are the fp64
+    values rounded fp64 -> fp32 -> bf16 (nearest even), as the oracle rounds."""
+    w = synth.named("tiny")
+    m32 = prep(w, 96, p=0.5, groups=G)
+    m16 = B.approx_lstm_prepare(w.W[:, :64], w.W[:, 64:], w.b, 64, 32, 96, prune_ratio=0.5, groups=G,
+                                flags=HOST, factor_dtype=1)
+    assert m16.info["factor_dtype"] == 1 and m32.info["factor_dtype"] == 0
+    for g in range(G):
+        a, b = B.approx_lstm_get_factors(m32, g), B.approx_lstm_get_factors(m16, g)
+        l64 = B.approx_lstm_get_factors_f64(m16, g)
+        assert np.array_equal(a["v_idx"], b["v_idx"])
+        assert np.array_equal(a["sigma"], b["sigma"])
+        assert np.array_equal(b["u"], oracle.round_bf16(l64["u"]).astype(np.float32))
+        vsel = np.take_along_axis(l64["v"], b["v_idx"].astype(np.int64), axis=1)
+        assert np.array_equal(b["v_val"], oracle.round_bf16(vsel).astype(np.float32))
+        assert not np.array_equal(a["u"], b["u"])
 
 
 def test_host_only_model_cannot_run():

@@ -355,6 +355,51 @@ def test_round_bf16_matches_torch():
     assert np.array_equal(oracle.round_bf16(a), ref)
 
 
+def test_bf16_operands_are_a_no_op_when_every_operand_is_representable():
+    """Batched bf16 configuration: rounding x~ and z to bf16 changes nothing
+    when they are already bf16 values.  Each gate is 4 u e_k^T with u having
+    entries +-1/2 (so sigma = 4, v = e_k, one kept entry) and x on a grid of
+    1/8: after one step the bf16-operand run, the plain run and the exact
+    LSTM coincide."""
+    D, H = 6, 4
+    W = np.zeros((4 * H, D + H))
+    signs = np.array([[1, -1, 1, 1], [-1, -1, 1, -1], [1, 1, -1, 1], [-1, 1, 1, 1]]) * 0.5
+    for g, k in enumerate([0, 2, 3, 5]):
+        W[g * H:(g + 1) * H, k] = 4.0 * signs[g]
+    b = np.array([0.125, -0.25, 0.5, 0.0] * 4)
+    x = np.array([[[0.125, -1.5, 2.0, 0.375, 0.0, -0.625]]])
+    f = oracle.prepare(W, H, 1, 1).rounded("bf16")
+    assert np.allclose(f.sigma, 4.0) and np.all(f.mask[:, 0, 0] == [0, 2, 3, 5])
+    h16, c16 = oracle.run(f, b, x, [1], operand_round="bf16")
+    h64, c64 = oracle.run(f, b, x, [1])
+    he, ce = oracle.exact_lstm(W, b, x)
+    assert np.array_equal(h16, h64) and np.array_equal(c16, c64)
+    np.testing.assert_allclose(h64[0], he, rtol=0, atol=1e-15)
+
+
+def test_bf16_operand_error_within_the_rounding_bound():
+    """Batched bf16 configuration, one timestep from h0 = c0 = 0: each
+    product takes three rounded quantities (v value, x~ entry, then z with u),
+    so |dy| <= ((1 + 2^-8)^3 - 1) * sum_n |sigma_n| |u_n| (|v'_n|^T |x~|) to first
+    order, with 2^-8 bounding bf16's relative rounding error; the cell update
+    then gives |dh| <= (1/4 + 1/4 + 1) max |dy| (sigmoid' <= 1/4, tanh' <= 1).
+    The bf16 mode must differ from the fp64 mode, and by no more than that."""
+    w = synth.named("tiny")
+    f = oracle.prepare(w.W, 32, 96, 48).rounded("bf16")
+    x1 = w.x[:1].astype(np.float64)
+    h16, _ = oracle.run(f, w.b, x1, [96], operand_round="bf16")
+    h64, _ = oracle.run(f, w.b, x1, [96])
+    xt = np.abs(np.concatenate([x1[0], np.zeros((1, 32))], axis=1))[0]
+    bound = np.zeros(128)
+    for g in range(4):
+        V = np.abs(oracle.dense_pruned_v(f, g))
+        bound[g * 32:(g + 1) * 32] = (np.abs(f.U[g]).T * np.abs(f.sigma[g])) @ (V @ xt)
+    u = 2.0 ** -8
+    dy = ((1 + u) ** 3 - 1) * bound
+    diff = np.abs(h16 - h64).max()
+    assert 0 < diff <= 1.5 * dy.max()
+
+
 def test_termination_and_degenerate_zero_matrix():
     """A zero gate matrix has no live terms (every sigma 0, output bias-only)."""
     D, H = 6, 2
