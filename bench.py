@@ -21,6 +21,7 @@ import time
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def algorithmic_bytes_per_timestep(G, Rg, NZ, C, K, D, H, B, L):
@@ -53,6 +54,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only time a plain 256 MiB device copy (reference for HBM counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--workload", default="driving", choices=["driving", "batched"],
+                    help="driving: batch 1, fp32 (default line); batched: 256 sequences, bf16 MFMA path")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -68,6 +71,9 @@ def main():
     from paper_1905_00689_amd import binding as B
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.workload == "batched":
+        bench_batched(args, torch)
+        return
     dev = torch.device("cuda")
     wl = synth.named("driving")
     D, H, T, Bn = wl.D, wl.H, wl.T, wl.B
@@ -168,6 +174,134 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def mfma_flops_batched(G, D, H, T, Bp, K):
+    """MFMA flops one batched run executes at budget K (dense zero-filled
+    panels; rows, D, H padded to the 32-wide MFMA contraction, sequences to
+    64): the x-projection once, then per timestep the h-projection and the U
+    accumulation of all four gates."""
+    r32 = lambda v: (v + 31) // 32 * 32
+    rows = G * r32(K)
+    xproj = 2 * rows * r32(D) * T * Bp
+    hproj = 2 * rows * r32(H) * Bp
+    accum = 2 * 4 * H * r32(K) * Bp
+    return xproj + T * (hproj + accum)
+
+
+def bench_batched(args, torch):
+    """The batched workload: 256 independent driving-shaped sequences (D=2048,
+    H=512, T=16), rank 512, 75% pruning, bf16 factors with fp32 accumulation
+    on MFMA.  A step is one approx_lstm_run over the batch at budget K."""
+    from paper_1905_00689_amd import synth
+    from paper_1905_00689_amd import binding as B
+    dev = torch.device("cuda")
+    wl = synth.named("batched")
+    D, H, T, Bn = wl.D, wl.H, wl.T, wl.B
+    rank = 512
+    t0 = time.time()
+    m = B.approx_lstm_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H, rank, prune_ratio=args.prune, groups=4,
+                              factor_dtype=1)
+    prep_s = time.time() - t0
+    info = m.info
+    NZ, G, Rg = info["nz"], info["groups"], info["rows_per_group"]
+    B.approx_lstm_reserve(m, T, Bn, 1)
+    x = torch.from_numpy(wl.x).to(dev)
+    h_out = torch.empty((1, T, Bn, H), device=dev)
+    stream = torch.cuda.current_stream()
+    Bp = (Bn + 63) // 64 * 64
+
+    def timed(K, steps, warmup):
+        for _ in range(warmup):
+            B.approx_lstm_run(m, x, [K], h_out, stream=stream)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            B.approx_lstm_run(m, x, [K], h_out, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        B.approx_lstm_check(m)
+        return e0.elapsed_time(e1) / steps
+
+    K = args.K
+    ms = timed(K, args.steps, args.warmup)
+    sweep = {"K": [], "us_per_timestep": [], "timesteps_per_s": [], "mfma_frac": []}
+    for k in (32, 128, 512):
+        msk = timed(k, args.sweep_steps, 5)
+        sweep["K"].append(k)
+        sweep["us_per_timestep"].append(round(msk * 1e3 / T, 4))
+        sweep["timesteps_per_s"].append(round(T * Bn / (msk * 1e-3), 1))
+        sweep["mfma_frac"].append(round(mfma_flops_batched(G, D, H, T, Bp, k) / (msk * 1e-3) / 1e12
+                                        / MFMA_BF16_PEAK_TFLOPS, 4))
+    flops = mfma_flops_batched(G, D, H, T, Bp, K)
+    algo = T * algorithmic_flops_per_timestep(G, Rg, NZ, K, Bn)
+    achieved = flops / (ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "kernel": "one step: batched_xproj_kernel + T x (batched_hproj_kernel + batched_accum_kernel)",
+                "flops_per_launch": flops, "algorithmic_flops_per_launch": algo,
+                "algorithmic_tflops": round(algo / (ms * 1e-3) / 1e12, 2)}
+    cpu = None if args.no_cpu_baseline else cpu_baseline_batched(m, wl, K, args.cpu_seconds)
+    out = {
+        "metric": "LSTM timesteps/sec at refinement budget K (and us/timestep vs K)",
+        "value": round(T * Bn / (ms * 1e-3), 1), "unit": "timesteps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"batched driving-shaped LSTM D=2048 H=512 T=16 B=256, per-gate rank 512, "
+                               f"{int(args.prune * 100)}% pruning (NZ={NZ}), bf16 factors, fp32 accumulation, K={K}",
+                   "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
+        "us_per_timestep": round(ms * 1e3 / T, 4), "prepare_s": round(prep_s, 2),
+        "sweep": sweep, "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_batched(m, wl, K, seconds):
+    """The float64 oracle (bf16 operand mode) on the library's exported terms,
+    over the whole sequence for a sample of the batch, repeated for about
+    `seconds`; the rate is timesteps of single sequences per second."""
+    import oracle
+    fac = exported_terms(m)
+    threads = oracle_threads()
+    sample = 8
+    xs = wl.x[:, :sample]
+    runs, t0 = 0, time.time()
+    while True:
+        oracle.run(fac, wl.b, xs, [K], operand_round="bf16")
+        runs += 1
+        el = time.time() - t0
+        if el >= seconds or runs >= 10000:
+            break
+    ts = runs * wl.T * sample
+    return {"value": round(ts / el, 2), "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"oracle.run (float64 NumPy, bf16 operand mode) over the full T={wl.T} sequence of "
+                      f"{sample} of the {wl.B} sequences at K={K}, repeated {runs} times ({el:.1f} s), "
+                      "on the library's exported terms"}
+
+
+def exported_terms(m):
+    """The library's stored terms as an oracle Factors object (timing only)."""
+    from oracle.factorise import Factors
+    from paper_1905_00689_amd import binding as B
+    inf = m.info
+    G, N, Rg, nz = inf["groups"], inf["rank"], inf["rows_per_group"], inf["nz"]
+    sig = np.zeros((G, N)); U = np.zeros((G, N, Rg)); mask = np.zeros((G, N, nz), np.int64)
+    vals = np.zeros((G, N, nz))
+    for g in range(G):
+        f = B.approx_lstm_get_factors(m, g)
+        sig[g], U[g], mask[g], vals[g] = f["sigma"], f["u"], f["v_idx"], f["v_val"]
+    return Factors(inf["input_size"], inf["hidden_size"], G, N, nz, sig, U, mask, vals,
+                   np.zeros((G, N, 1)), np.array(inf["eff_rank"]), "bf16" if inf["factor_dtype"] else "f32")
+
+
+def oracle_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:
+        return os.cpu_count()
+
+
 def measured_traffic():
     """HBM bytes per step from the committed rocprofv3 counter summary, if it
     was taken on the kernel source as it is now (else None)."""
@@ -210,22 +344,8 @@ def cpu_baseline(m, wl, K, seconds):
     oracle runs on the library's exported terms (timing only: values do not
     change its cost)."""
     import oracle
-    from oracle.factorise import Factors
-    from paper_1905_00689_amd import binding as B
-    inf = m.info
-    G, N, Rg, nz, C = inf["groups"], inf["rank"], inf["rows_per_group"], inf["nz"], inf["aug_size"]
-    sig = np.zeros((G, N)); U = np.zeros((G, N, Rg)); mask = np.zeros((G, N, nz), np.int64)
-    vals = np.zeros((G, N, nz))
-    for g in range(G):
-        f = B.approx_lstm_get_factors(m, g)
-        sig[g], U[g], mask[g], vals[g] = f["sigma"], f["u"], f["v_idx"], f["v_val"]
-    fac = Factors(inf["input_size"], inf["hidden_size"], G, N, nz, sig, U, mask, vals,
-                  np.zeros((G, N, 1)), np.array(inf["eff_rank"]), "f32")
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count()
+    fac = exported_terms(m)
+    threads = oracle_threads()
     runs, t0 = 0, time.time()
     while True:
         oracle.run(fac, wl.b, wl.x, [K])

@@ -132,8 +132,8 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
  * the projections is shared.  With a bf16 model (factor_dtype 1) every
  * product takes bf16 operands -- x~ = [x_t; h_{t-1}], the factor values and
  * z = sigma * (prune(v)^T x~) -- with fp32 accumulation; h_out and c_out stay
- * fp32; sequences are padded to a multiple of 64 internally (B <= 2^20 and
- * T * padded B <= 2^30, else UNSUPPORTED).  Asynchronous on hip_stream; the call blocks
+ * fp32; sequences are padded to a multiple of 64 internally (B <= 2^20,
+ * T * padded B <= 2^30 and T * B * D < 2^31, else UNSUPPORTED).  Asynchronous on hip_stream; the call blocks
  * only to allocate workspace on first use (see approx_lstm_reserve).  The
  * device-side waits of the kernel are bounded; if one expires the next
  * approx_lstm_check call reports APPROX_LSTM_ERR_DEVICE.

@@ -84,7 +84,10 @@ struct approx_lstm_model {
   uint16_t* d_nx = nullptr;
   uint64_t dev_bytes = 0;
   int num_cu = 0;
-  // bf16 panel store (factor_dtype 1): Vx [prow][Dp], Vh [prow][Hp], Ut [4H][Kp]
+  // bf16 panel store (factor_dtype 1): Vx [prow][Dp], Vh [prow][Hp], Ut [4H][Kp];
+  // Dp = D rounded up to 64, Hp, Kp = H, rank rounded up to 32 (the MFMA
+  // contraction step), prow = G*Kp rounded up to 128 (the x-projection's row
+  // tile)
   int dtype = 0;
   int Dp = 0, Hp = 0, Kp = 0, prow = 0;
   uint16_t* d_Vx = nullptr;
@@ -220,7 +223,14 @@ approx_lstm_status ensure_batched(approx_lstm_model* m, int T, size_t Bp, int km
   const size_t prows = (size_t)m->G * round_up((size_t)kmax, 32);
   approx_lstm_status st = grow(m->d_px, m->px_cap, std::max<size_t>(1, prows * T * Bp), stream, "hipMalloc(P)");
   if (st == APPROX_LSTM_OK) st = grow(m->d_bz, m->bz_cap, (size_t)m->G * Bp * m->Kp, stream, "hipMalloc(Z)");
-  if (st == APPROX_LSTM_OK) st = grow(m->d_bh, m->bh_cap, Bp * m->Hp, stream, "hipMalloc(hb)");
+  if (st == APPROX_LSTM_OK && Bp * m->Hp > m->bh_cap) {
+    // the padding columns of hb (units H..Hp-1) are never written by a run:
+    // they must hold zeros (bf16 +0) from allocation on
+    st = grow(m->d_bh, m->bh_cap, Bp * m->Hp, stream, "hipMalloc(hb)");
+    if (st == APPROX_LSTM_OK)
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_bh), m->bh_cap / 4, stream),
+              "clear(hb)");
+  }
   if (st == APPROX_LSTM_OK) st = grow(m->d_bc, m->bc_cap, Bp * m->H, stream, "hipMalloc(c)");
   return st;
 }
@@ -229,10 +239,12 @@ approx_lstm_status ensure_batched(approx_lstm_model* m, int T, size_t Bp, int km
 approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int B, const float* h0, const float* c0,
                                const int32_t* levels, int n_levels, float* h_out, float* c_out,
                                hipStream_t stream) {
-  const size_t Bp = round_up((size_t)B, 64);
+  const size_t Bp = round_up((size_t)B, alstm::kBatchAlign);
   if (Bp > ((size_t)1 << 20)) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "B = %d exceeds 2^20 for a bf16 model", B);
   if ((size_t)T * Bp > (size_t)1 << 30)
     return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T * padded B = %zu exceeds 2^30", (size_t)T * Bp);
+  if ((size_t)T * B * m->D >= ((size_t)1 << 31))
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T * B * D = %zu reaches 2^31", (size_t)T * B * m->D);
   int kmax = 0;
   for (int l = 0; l < n_levels; ++l) kmax = std::max(kmax, (int)levels[l]);
   approx_lstm_status st = ensure_batched(m, T, Bp, kmax, stream);
@@ -383,10 +395,10 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
     std::vector<uint16_t> vx16, vh16, ut16;
     const bool bf = m->dtype == 1;
     if (bf) {
-      m->Dp = (int)round_up(D, 32);
-      m->Hp = (int)round_up(H, 32);
-      m->Kp = (int)round_up(N, 32);
-      m->prow = (int)round_up((size_t)G * m->Kp, 64);
+      m->Dp = (int)round_up(D, alstm::kPanelDAlign);
+      m->Hp = (int)round_up(H, alstm::kPanelAlign);
+      m->Kp = (int)round_up(N, alstm::kPanelAlign);
+      m->prow = (int)round_up((size_t)G * m->Kp, alstm::kPanelRowAlign);
       vx16.assign((size_t)m->prow * m->Dp, 0);
       vh16.assign((size_t)m->prow * m->Hp, 0);
       ut16.assign((size_t)4 * H * m->Kp, 0);
@@ -451,7 +463,7 @@ approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int3
   if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
   approx_lstm_status st;
   if (m->dtype == 1) {
-    st = ensure_batched(m, T_max, round_up((size_t)B_max, 64), m->N, nullptr);
+    st = ensure_batched(m, T_max, round_up((size_t)B_max, alstm::kBatchAlign), m->N, nullptr);
     if (st != APPROX_LSTM_OK) return st;
     HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
     return APPROX_LSTM_OK;

@@ -85,8 +85,8 @@ hipError_t launch_clear_u64(unsigned long long* p, size_t n, hipStream_t stream)
 
 // Batched bf16 path (many sequences; the factors as zero-filled bf16 panels
 // and every product on MFMA with fp32 accumulation).  bf16 arrays are raw
-// 16-bit patterns.  Padded sizes: Dp, Hp multiples of 32; Bp a multiple of 64;
-// Kp = rank rounded up to 32; panel rows = G*Kp rounded up to 64.
+// 16-bit patterns.  Padded sizes: Dp a multiple of 64, Hp of 32, Bp of 64;
+// Kp = rank rounded up to 32; panel rows = G*Kp rounded up to 128.
 //   x      [T][B][D] fp32           h0, c0 [B][H] fp32 or null
 //   h_out  [L][T][B][H]             c_out  [L][B][H] or null
 //   sigma  [N*G] fp32               term tau = n*G + g
@@ -94,10 +94,15 @@ hipError_t launch_clear_u64(unsigned long long* p, size_t n, hipStream_t stream)
 //   Vh     [rows][Hp] bf16          h-part of prune(v) of term tau
 //   Ut     [4H][Kp] bf16            Ut[o][n] = u of term (n, g(o)) at row o within its group
 //   bias   [4H] fp32
-//   P      [rows_used][T*Bp] fp32   x-part projections, column t*Bp + b (workspace)
+//   P      [T*Bp][pld] fp32         x-part projections: P[t*Bp + b][tau] (workspace)
 //   Z      [G][Bp][Kp] bf16         sigma * s of the current timestep (workspace)
 //   hb     [Bp][Hp] bf16            h of the previous timestep (workspace)
 //   c      [Bp][H] fp32             cell state (workspace)
+constexpr int kPanelAlign = 32;      // Hp, Kp granularity (the MFMA contraction step)
+constexpr int kPanelDAlign = 64;     // Dp granularity (two x-projection slices)
+constexpr int kPanelRowAlign = 128;  // panel row granularity (the x-projection row tile)
+constexpr int kBatchAlign = 64;      // Bp granularity
+
 struct BatchedArgs {
   const float* x;
   const float* h0;
@@ -115,6 +120,7 @@ struct BatchedArgs {
   float* c;
   int D, Dp, H, Hp, G, Kp, T, B, Bp;
   int rows;        // panel rows a launch covers (set per launch)
+  int pld;         // row count of P: G * (largest level rounded up to 32)
   int xvec;        // 1: x rows may be read as 16-byte vectors (D % 4 == 0, x 16-byte aligned)
 };
 
