@@ -54,6 +54,7 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only time a plain 256 MiB device copy (reference for HBM counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--batched-sweep", default="32,128,512", help="K values timed in the batched workload")
     ap.add_argument("--workload", default="driving", choices=["driving", "batched"],
                     help="driving: batch 1, fp32 (default line); batched: 256 sequences, bf16 MFMA path")
     args = ap.parse_args()
@@ -151,7 +152,7 @@ def main():
     achieved = bytes_launch / (ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": measured_traffic() if (K == 512 and abs(args.prune - 0.75) < 1e-9) else None,
+                "traffic": measured_traffic("driving") if (K == 512 and abs(args.prune - 0.75) < 1e-9) else None,
                 "kernel": "one step: input_proj_kernel + progressive_lstm_kernel",
                 "bytes_per_launch": bytes_launch,
                 "flops_per_launch": T * algorithmic_flops_per_timestep(G, Rg, NZ, K, Bn)}
@@ -226,7 +227,7 @@ def bench_batched(args, torch):
     K = args.K
     ms = timed(K, args.steps, args.warmup)
     sweep = {"K": [], "us_per_timestep": [], "timesteps_per_s": [], "mfma_frac": []}
-    for k in (32, 128, 512):
+    for k in [int(v) for v in args.batched_sweep.split(",") if v]:
         msk = timed(k, args.sweep_steps, 5)
         sweep["K"].append(k)
         sweep["us_per_timestep"].append(round(msk * 1e3 / T, 4))
@@ -237,7 +238,8 @@ def bench_batched(args, torch):
     algo = T * algorithmic_flops_per_timestep(G, Rg, NZ, K, Bn)
     achieved = flops / (ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+                "traffic": measured_traffic("batched") if (K == 512 and abs(args.prune - 0.75) < 1e-9) else None,
                 "kernel": "one step: batched_xproj_kernel + T x (batched_hproj_kernel + batched_accum_kernel)",
                 "flops_per_launch": flops, "algorithmic_flops_per_launch": algo,
                 "algorithmic_tflops": round(algo / (ms * 1e-3) / 1e12, 2)}
@@ -302,13 +304,20 @@ def oracle_threads():
         return os.cpu_count()
 
 
-def measured_traffic():
-    """HBM bytes per step from the committed rocprofv3 counter summary, if it
-    was taken on the kernel source as it is now (else None)."""
+TRAFFIC_PROFILES = {
+    "driving": ("driving_K512_p75_hbm_counters.md", "kernels.hip"),
+    "batched": ("batched_K512_p75_hbm_counters.md", "batched.hip"),
+}
+
+
+def measured_traffic(workload):
+    """HBM bytes per step from the committed rocprofv3 counter summary of the
+    workload, if it was taken on the kernel source as it is now (else None)."""
     import hashlib
     root = os.path.dirname(os.path.abspath(__file__))
-    prof = os.path.join(root, "profiles", "driving_K512_p75_hbm_counters.md")
-    src = os.path.join(root, "paper_1905_00689_amd", "csrc", "kernels.hip")
+    prof_name, src_name = TRAFFIC_PROFILES[workload]
+    prof = os.path.join(root, "profiles", prof_name)
+    src = os.path.join(root, "paper_1905_00689_amd", "csrc", src_name)
     try:
         fields = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if ": " in l and not l.startswith(" "))
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
