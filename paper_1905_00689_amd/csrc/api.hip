@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -107,6 +108,10 @@ struct approx_lstm_model {
   size_t zx_cap = 0;                 // words
   unsigned long long* d_hx = nullptr;
   size_t hx_cap = 0;
+  float* d_hbx = nullptr;            // bulk h exchange, [2][hb_stride]
+  size_t hbx_cap = 0;                // floats
+  unsigned* d_hflag = nullptr;       // bulk h exchange flags, one per workgroup
+  size_t hflag_cap = 0;
   unsigned* d_err = nullptr;
   unsigned long long* d_stamps = nullptr;
   size_t stamps_cap = 0;             // words
@@ -123,7 +128,9 @@ struct approx_lstm_model {
   int cooperative = 0;               // 1: cooperative launch API
 
   ~approx_lstm_model() {
-    if (!has_dev && !d_px && !d_zx && !d_hx && !d_err && !d_stamps && !d_stack && !d_bz && !d_bh && !d_bc) return;
+    if (!has_dev && !d_px && !d_zx && !d_hx && !d_hbx && !d_hflag && !d_err && !d_stamps && !d_stack && !d_bz &&
+        !d_bh && !d_bc)
+      return;
     DeviceScope ds(device);
     dfree(d_Vx);
     dfree(d_Vh);
@@ -140,6 +147,8 @@ struct approx_lstm_model {
     dfree(d_px);
     dfree(d_zx);
     dfree(d_hx);
+    dfree(d_hbx);
+    dfree(d_hflag);
     dfree(d_err);
     dfree(d_stamps);
     dfree(d_stack);
@@ -235,6 +244,21 @@ approx_lstm_status ensure_batched(approx_lstm_model* m, int T, size_t Bp, int km
   return st;
 }
 
+// Bulk h exchange buffers: `floats` for the two parities of h_t and one flag
+// word per possible workgroup (cleared when new, so no stale tag can match).
+approx_lstm_status ensure_bulk(approx_lstm_model* m, size_t floats, hipStream_t stream) {
+  approx_lstm_status st = grow(m->d_hbx, m->hbx_cap, floats, stream, "hipMalloc(hbx)");
+  if (st != APPROX_LSTM_OK) return st;
+  const size_t flags = round_up((size_t)std::max(1, m->num_cu), 2);
+  if (flags > m->hflag_cap) {
+    st = grow(m->d_hflag, m->hflag_cap, flags, stream, "hipMalloc(hflag)");
+    if (st != APPROX_LSTM_OK) return st;
+    HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
+            "clear(hflag)");
+  }
+  return APPROX_LSTM_OK;
+}
+
 // The batched bf16 run (factor_dtype 1): arguments already checked.
 approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int B, const float* h0, const float* c0,
                                const int32_t* levels, int n_levels, float* h_out, float* c_out,
@@ -263,9 +287,11 @@ approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int 
 
 // Workgroups for a run: about one per 32 terms in use (so that every
 // workgroup's terms and rows fit registers), at most 256.
-int auto_blocks(const approx_lstm_model* m, int GK) {
+int auto_blocks(const approx_lstm_model* m, int GK, int LB) {
   int cap = std::max(1, std::min(m->num_cu, 256));
-  int want = (GK + 31) / 32;
+  // without terms the workgroups are independent (no exchange): spread the
+  // cell updates, about 256 (unit, sequence) pairs per workgroup
+  int want = GK > 0 ? (GK + 31) / 32 : (int)(((long long)m->H * LB + 255) / 256);
   return std::max(1, std::min(cap, want));
 }
 
@@ -314,9 +340,13 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
     }
     alstm::FactoriseOptions opt;
     opt.keep_unpruned = keep;
-    // groups run on their own threads; the rest of the host's cores split the
-    // row loops inside each group
-    const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+    // groups run on their own threads; the host's thread budget (OMP_NUM_THREADS
+    // when set, else the hardware's) is split over the row loops of the groups
+    unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+    if (const char* env = std::getenv("OMP_NUM_THREADS")) {
+      const long v = std::strtol(env, nullptr, 10);
+      if (v > 0) hw = std::min<unsigned>(hw, (unsigned)v);
+    }
     opt.threads = std::max(1, (int)(hw / (unsigned)G));
     std::vector<std::thread> th;
     for (int g = 0; g < G; ++g)
@@ -471,6 +501,8 @@ approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int3
   const size_t GK = (size_t)m->G * m->N, LB = (size_t)L_max * B_max;
   const size_t P_max = std::max(1, m->num_cu);
   st = ensure_workspace(m, GK * T_max * B_max, LB * (GK + P_max), LB * m->H, nullptr);
+  if (st == APPROX_LSTM_OK && alstm::use_bulk_h(L_max, B_max, m->H))
+    st = ensure_bulk(m, 2 * round_up(LB * m->H, 4), nullptr);
   if (st != APPROX_LSTM_OK) return st;
   HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
   return APPROX_LSTM_OK;
@@ -509,7 +541,7 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   a.lanes_a = alstm::lanes_for_terms(m->NZ, m->D, m->H);
   for (int l = 0; l < n_levels; ++l) a.lanes_b[l] = alstm::lanes_for_level(levels[l]);
   const int maxP = std::max(1, m->num_cu);
-  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK);
+  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK, n_levels * B);
   size_t lds = alstm::plan_progressive(a, P);
   if (m->launch_blocks == 0)   // automatic: widen until the per-workgroup slices fit in LDS
     while (lds > alstm::kLdsCap && P < maxP) {
@@ -525,17 +557,28 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
       ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * P * a.owned_max),
                        LB * m->H, stream);
   if (st != APPROX_LSTM_OK) return st;
+  a.bulk_h = alstm::use_bulk_h(n_levels, B, m->H);
+  a.hb_stride = (int)round_up(LB * m->H, 4);
+  if (a.bulk_h) {
+    st = ensure_bulk(m, 2 * (size_t)a.hb_stride, stream);
+    if (st != APPROX_LSTM_OK) return st;
+  }
   m->seq = (m->seq + 1) & 0xFFFFu;
   if (m->seq == 0) {
     // tag space wrapped: clear the exchange words so no stale tag can match
     HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
     HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+    if (m->d_hflag)
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
+              "clear(hflag)");
     m->seq = 1;
   }
   a.tag_base = m->seq << 16;
   a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
   a.sigma = m->d_sigma; a.Ut = m->d_Ut; a.vidx = m->d_vidx; a.vval = m->d_vval; a.nx = m->d_nx;
   a.bias = m->d_bias; a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx; a.err = m->d_err;
+  a.hbx = a.bulk_h ? m->d_hbx : nullptr;
+  a.hflag = a.bulk_h ? m->d_hflag : nullptr;
   a.stamps = nullptr;
   if (m->timing) {
     const size_t words = 4 + 4 * (size_t)T;

@@ -203,9 +203,62 @@ __device__ __forceinline__ void gather_level_any(float* zs, const uint16_t* slot
   const int per = (nslots + nthr - 1) / nthr;     // slots per thread for a single pass
   if (per <= 1) gather_level<1>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
   else if (per <= 2) gather_level<2>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
-  else if (per <= 3) gather_level<3>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
-  else if (per <= 5) gather_level<5>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+  else if (per <= 4) gather_level<4>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
   else gather_level<8>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+}
+
+// Bulk h exchange.  The publisher wave stores its h values with agent-scope
+// (sc1, write-through) stores, waits until the wave's stores are acknowledged
+// (vmcnt 0), then stores its tag in its flag word.  Readers poll every workgroup's flag, then
+// read the whole h_t with agent-scope 16-byte loads; coherent across XCDs
+// without any cache writeback or invalidation.
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(reinterpret_cast<unsigned*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// threads tid < nthr poll flags [0, P) until each holds `tag` (bounded)
+__device__ __forceinline__ void await_flags(const unsigned* flag, int P, unsigned tag, unsigned* err, int tid,
+                                            int nthr) {
+  for (int f = tid; f < P; f += nthr) {
+    unsigned spins = 0;
+    while (__hip_atomic_load(flag + f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != tag) {
+      __builtin_amdgcn_s_sleep(2);
+      if ((++spins & 255u) == 0u &&
+          (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+    }
+  }
+}
+
+// dst[i] = src[i] for i < n (src 16-byte aligned, readable up to n rounded up
+// to 4), agent-scope loads, 4 in flight per thread
+__device__ __forceinline__ void read_coherent(float* dst, const float* src, int n, int tid, int nthr) {
+  typedef float f32x4_t __attribute__((ext_vector_type(4)));
+  // the buffer descriptor must be wave-uniform (scalar registers)
+  const unsigned long long addr = reinterpret_cast<unsigned long long>(src);
+  const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)addr);
+  const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(addr >> 32));
+  const int n4 = __builtin_amdgcn_readfirstlane((n + 3) >> 2);
+  float* base = reinterpret_cast<float*>(((unsigned long long)hi << 32) | lo);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(base, (short)0, n4 * 16, 0x00020000);
+  for (int base = 0; base < n4; base += 4 * nthr) {
+    f32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i4 = base + u * nthr + tid;
+      v[u] = __builtin_amdgcn_raw_buffer_load_b128(rs, (i4 < n4 ? i4 : 0) * 16, 0, 16 /* sc1 */);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i4 = base + u * nthr + tid;
+      if (i4 < n4)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          if (4 * i4 + c < n) dst[4 * i4 + c] = v[u][c];
+    }
+  }
 }
 
 // Workgroup barrier that orders LDS only.  __syncthreads() would also wait
@@ -549,6 +602,9 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
       }
     }
     if (stamp) a.stamps[5 + 4 * t] = clock64();
+    // without terms (every level K = 0) no workgroup reads another's h
+    const bool exch = !local && GK > 0;
+    float* hbt = a.bulk_h ? a.hbx + (size_t)(t & 1) * a.hb_stride : nullptr;
     if (publisher) {
       for (int lb = 0; lb < LB; ++lb) {
         const int l = lb / B, b = lb % B;
@@ -556,13 +612,31 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           const float h2 = hown[lb * RP + rr];
           const int r = r0 + rr;
           a.h_out[(((size_t)l * T + t) * B + b) * H + r] = h2;
-          if (!local) publish(a.hx + (size_t)lb * H + r, h2, tag);
+          if (exch) {
+            if (a.bulk_h) store_coherent(hbt + (size_t)lb * H + r, h2);
+            else publish(a.hx + (size_t)lb * H + r, h2, tag);
+          }
         }
+      }
+      if (exch && a.bulk_h) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's h stores acknowledged
+        if (lane == 0) __hip_atomic_store(a.hflag + j, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
 
     // ---- phase C: gather h_t ----
-    if (!local && !publisher) gather_tagged<2>(hs, nullptr, a.hx, LB * H, tag, a.err, threadIdx.x, gthr);
+    if (exch) {
+      if (a.bulk_h) {
+        // h_t is double-buffered by step parity: a workgroup can publish
+        // h_{t+1} only after every z of step t+1, i.e. after every workgroup
+        // has finished reading h_t
+        if (!publisher) await_flags(a.hflag, P, tag, a.err, threadIdx.x, gthr);
+        lds_barrier();
+        if (!publisher) read_coherent(hs, hbt, LB * H, threadIdx.x, gthr);
+      } else if (!publisher) {
+        gather_tagged<2>(hs, nullptr, a.hx, LB * H, tag, a.err, threadIdx.x, gthr);
+      }
+    }
     lds_barrier();
   }
   if (stamp) {
@@ -771,9 +845,9 @@ size_t plan_progressive(RunArgs& a, int P) {
     else if (need_o <= 4 && need_u <= 8) { a.opt = 4; a.upt = 8; }
     if (a.opt == 1 && need_u <= 8) a.upt = 8;
     else if (a.opt == 1 && need_u <= 16) a.upt = 16;
-    // 64 U entries per thread only next to at most 12 h-part entries per
+    // 64 U entries per thread only next to at most 8 h-part entries per
     // lane: beyond that the register file (256 per lane) spills
-    if (a.upt == 64 && a.hpl > 12) { a.opt = 0; a.upt = 0; }
+    if (a.upt == 64 && a.hpl > 8) { a.opt = 0; a.upt = 0; }
   }
   a.P = P;
   a.vh_lds = 0;
@@ -818,7 +892,7 @@ hipError_t launch_u(const RunArgs& a, int blocks, int cooperative, size_t lds, h
   if (a.opt == 1 && a.upt == 8) return launch_one<HPL, 1, 8>(a, blocks, cooperative, lds, stream);
   if (a.opt == 1 && a.upt == 16) return launch_one<HPL, 1, 16>(a, blocks, cooperative, lds, stream);
   if (a.opt == 1 && a.upt == 32) return launch_one<HPL, 1, 32>(a, blocks, cooperative, lds, stream);
-  if constexpr (HPL <= 12)
+  if constexpr (HPL <= 8)
     if (a.opt == 1 && a.upt == 64) return launch_one<HPL, 1, 64>(a, blocks, cooperative, lds, stream);
   if (a.opt == 2) return launch_one<HPL, 2, 16>(a, blocks, cooperative, lds, stream);
   if (a.opt == 4) return launch_one<HPL, 4, 8>(a, blocks, cooperative, lds, stream);

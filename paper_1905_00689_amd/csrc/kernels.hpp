@@ -24,7 +24,8 @@ constexpr size_t kLdsCap = 160 * 1024; // LDS per CU on gfx950
 //   px     [GK][T*B]            x-part projections (workspace, written by input_proj_kernel)
 //   zx     [L*B][P][owned_max] u64  tagged z exchange (value | tag << 32), slot
 //                                   j*owned_max + i carries term j + i*P
-//   hx     [L*B][H] u64         tagged h exchange
+//   hx     [L*B][H] u64         tagged h exchange (few values per workgroup)
+//   hbx, hflag                  bulk h exchange (many values: large L*B*H)
 struct RunArgs {
   const float* x;
   const float* h0;
@@ -40,6 +41,9 @@ struct RunArgs {
   float* px;
   unsigned long long* zx;
   unsigned long long* hx;
+  float* hbx;      // bulk h exchange: [2][hb_stride] floats, h_t of every (level, seq) at
+                   // parity t & 1 (agent-coherent stores and loads); null unless bulk_h
+  unsigned* hflag; // bulk h exchange: [P] words, workgroup j's tag once its h_t is stored
   unsigned* err;
   unsigned long long* stamps;  // null, or [4 + 4T] stamps written by workgroup 0: [0] wall clock
                                // and [1] shader clock at the start of the recurrence; shader
@@ -57,6 +61,8 @@ struct RunArgs {
   int opt;         // output rows per thread in the register path
   int ustride;     // LDS row stride (floats) of the resident U slice; 0 = U read from global
   int px_all;      // 1: x-part projections of every timestep resident in LDS
+  int bulk_h;      // 1: h exchanged in bulk (hbx + hflag), 0: as tagged words (hx)
+  int hb_stride;   // floats per parity of hbx: L*B*H rounded up to 4
   int P;           // workgroups of the launch
   int lanes_a;     // lanes per term in phase A (16)
   unsigned tag_base;
@@ -69,6 +75,11 @@ struct RunArgs {
 // levels of a run, so every result has one fixed summation order.
 int lanes_for_terms(int nz, int D, int H);
 int lanes_for_level(int K);
+
+// 1 when the h_t of a launch (L*B*H values) is exchanged in bulk: the
+// tagged-word gather needs one polling round per 2 values per thread, the
+// bulk one a flag round and one 16-byte load per 4 values.
+inline int use_bulk_h(int L, int B, int H) { return (long long)L * B * H > 2048 ? 1 : 0; }
 
 // Fills the launch-shape fields (rows_per .. lanes_a) for P workgroups and
 // returns the LDS bytes the kernel then needs (> kLdsCap: does not fit).

@@ -144,6 +144,40 @@ def test_driving_levels_are_bitwise_independent(driving, driving_p75):
         assert np.array_equal(together[j], alone[0]), K
 
 
+def test_bulk_and_tagged_h_exchange_agree_bitwise(driving, driving_p75):
+    """Five levels of the driving workload exchange h in bulk (5 x 512 values
+    per timestep: flag words and coherent 16-byte loads); one level exchanges
+    tagged words.  The values exchanged are the same, so every level must
+    match its single-level run bit for bit (and the oracle)."""
+    levels = [64, 64, 512, 8, 64]
+    say("driving: bulk h exchange (5 levels) vs tagged (1 level)")
+    together, _ = run_gpu(driving_p75, driving.x, levels)
+    for j, K in enumerate(levels):
+        alone, _ = run_gpu(driving_p75, driving.x, [K])
+        assert np.array_equal(together[j], alone[0]), (j, K)
+
+
+def test_zero_budget_spreads_over_workgroups():
+    """K = 0 (bias-only gates, Eq. (1) with no step) with 20 sequences: the
+    workgroups need nothing from each other; any launch width gives the same
+    bits, equal to the oracle."""
+    w = synth.make(64, 32, 6, 20, index=16, xkind="normal")
+    m = prep(w, 8, 0.5)
+    f = oracle.prepare(w.W, 32, 8, 48)
+    say("K = 0 over 20 sequences, launch widths")
+    ref = None
+    for P in (0, 1, 3, 8):
+        B.approx_lstm_set_launch(m, P, 0)
+        h, c = run_gpu(m, w.x, [0], want_c=True)
+        ho, co = oracle.run(f, w.b, w.x, [0])
+        assert rel_err(h, ho) < TOL, P
+        assert np.abs(c - co).max() < TOL * max(1.0, np.abs(co).max())
+        if ref is None:
+            ref = h
+        else:
+            assert np.array_equal(h, ref), P
+
+
 def test_driving_full_rank_without_pruning_is_the_exact_lstm(driving):
     say("driving p=0 rank 512 vs exact LSTM")
     m = prep(driving, 512, 0.0)
@@ -256,3 +290,68 @@ def test_deadline_infeasible(deadline_small):
     with pytest.raises(B.ApproxLstmError) as ei:
         B.approx_lstm_run_deadline(m, xt, 1e-3, h)
     assert ei.value.status == B.ERR_DEADLINE_INFEASIBLE
+
+
+# ------------------------------------------------------- full-size workloads
+def test_stack_full_size_matches_oracle_on_exported_terms():
+    """The stacked workload at its full size: D=4096 -> H=1024 -> H=1024,
+    T=32, batch 1, rank 1024 per layer, 75% pruning, per-layer budgets
+    (64, 64), (256, 256), (1024, 1024); every output against the oracle run
+    layer by layer on the library's exported terms."""
+    w = synth.named("stack")
+    (W1, b1), (W2, b2) = w.layers
+    levels = [(64, 64), (256, 256), (1024, 1024)]
+    say("stack full size: prepare layer 1 (4 gates of 1024 x 5120, rank 1024)")
+    m1 = B.approx_lstm_prepare(W1[:, :4096], W1[:, 4096:], b1, 4096, 1024, 1024, prune_ratio=0.75)
+    say("stack full size: prepare layer 2 (rank 1024)")
+    m2 = B.approx_lstm_prepare(W2[:, :1024], W2[:, 1024:], b2, 1024, 1024, 1024, prune_ratio=0.75)
+    say("stack full size: run levels", levels)
+    xt = torch.from_numpy(w.x).cuda()
+    h = torch.full((len(levels), 32, 1, 1024), float("nan"), device="cuda")
+    B.approx_lstm_run_stack([m1, m2], xt, levels, h)
+    B.approx_lstm_check(m1)
+    B.approx_lstm_check(m2)
+    torch.cuda.synchronize()
+    say("stack full size: oracle")
+    ho = oracle_stack([exported_factors(m1), exported_factors(m2)], [b1, b2], w.x, levels)
+    hg = h.cpu().numpy()
+    for j, lv in enumerate(levels):
+        e = rel_err(hg[j], ho[j])
+        say("  levels", lv, "rel err", e)
+        assert e < TOL, (lv, e)
+
+
+def test_deadline_full_shape_reduced_rank():
+    """The deadline workload's shapes (D=2048, H=2048, T=64, batch 8, 90%
+    pruning) with rank 256 instead of 2048 (the host factorisation at rank
+    2048 takes minutes): deadlines 5, 20 and 100 us per timestep; each run
+    that is feasible must equal the oracle replayed at the achieved budgets;
+    its error against the exact LSTM is reported."""
+    w = synth.named("deadline")
+    say("deadline shape: prepare rank 256")
+    m = B.approx_lstm_prepare(w.W[:, :2048], w.W[:, 2048:], w.b, 2048, 2048, 256, prune_ratio=0.9)
+    f = exported_factors(m)
+    xt = torch.from_numpy(w.x).cuda()
+    say("deadline shape: exact LSTM (oracle)")
+    he, _ = oracle.exact_lstm(w.W, w.b, w.x)
+    ks = []
+    for dl in (5.0, 20.0, 100.0):
+        h = torch.full((64, 8, 2048), float("nan"), device="cuda")
+        try:
+            k, us = B.approx_lstm_run_deadline(m, xt, dl, h)
+        except B.ApproxLstmError as e:
+            assert e.status == B.ERR_DEADLINE_INFEASIBLE
+            say("  deadline", dl, "us: infeasible:", str(e))
+            ks.append(-1)
+            continue
+        torch.cuda.synchronize()
+        assert np.all(k == k[0]) and 0 <= k[0] <= 256
+        ks.append(int(k[0]))
+        ho, _ = oracle.run_schedule(f, w.b, w.x, list(k))
+        hg = h.cpu().numpy()
+        e = rel_err(hg, ho)
+        say("  deadline", dl, "us: K", int(k[0]), "median step us", float(np.median(us)),
+            "rel err vs oracle", e, "max |h - exact| / max |exact|",
+            float(np.abs(hg - he).max() / np.abs(he).max()))
+        assert e < TOL, dl
+    assert ks == sorted(ks) and ks[-1] == 256
