@@ -575,6 +575,7 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   }
   a.tag_base = m->seq << 16;
   a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
+  a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
   a.sigma = m->d_sigma; a.Ut = m->d_Ut; a.vidx = m->d_vidx; a.vval = m->d_vval; a.nx = m->d_nx;
   a.bias = m->d_bias; a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx; a.err = m->d_err;
   a.hbx = a.bulk_h ? m->d_hbx : nullptr;

@@ -203,7 +203,8 @@ __device__ __forceinline__ void gather_level_any(float* zs, const uint16_t* slot
   const int per = (nslots + nthr - 1) / nthr;     // slots per thread for a single pass
   if (per <= 1) gather_level<1>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
   else if (per <= 2) gather_level<2>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
-  else if (per <= 4) gather_level<4>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+  else if (per <= 3) gather_level<3>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
+  else if (per <= 5) gather_level<5>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
   else gather_level<8>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
 }
 
@@ -696,7 +697,7 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
   for (int cb = 0; cb < TB; cb += xchunk) {
     const int cnt = min(xchunk, TB - cb);
     __syncthreads();
-    if ((D & 3) == 0 && xchunk == kMaxXChunk) {
+    if (a.xvec && xchunk == kMaxXChunk) {
       // lane (c, k4) loads x[cb+c][4k4 .. 4k4+3]; a wave's 64 writes of one
       // component land in 64 distinct banks (row stride 20 = 16 + 4)
       const int n = kMaxXChunk * (D >> 2);

@@ -61,6 +61,7 @@ struct RunArgs {
   int opt;         // output rows per thread in the register path
   int ustride;     // LDS row stride (floats) of the resident U slice; 0 = U read from global
   int px_all;      // 1: x-part projections of every timestep resident in LDS
+  int xvec;        // 1: x rows may be read as 16-byte vectors (D % 4 == 0, x 16-byte aligned)
   int bulk_h;      // 1: h exchanged in bulk (hbx + hflag), 0: as tagged words (hx)
   int hb_stride;   // floats per parity of hbx: L*B*H rounded up to 4
   int P;           // workgroups of the launch
