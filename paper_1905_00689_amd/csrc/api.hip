@@ -287,11 +287,13 @@ approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int 
 
 // Workgroups for a run: about one per 32 terms in use (so that every
 // workgroup's terms and rows fit registers), at most 256.
-int auto_blocks(const approx_lstm_model* m, int GK, int LB) {
+int auto_blocks(const approx_lstm_model* m, int GK, int LB, int LB_seq) {
   int cap = std::max(1, std::min(m->num_cu, 256));
   // without terms the workgroups are independent (no exchange): spread the
   // cell updates, about 256 (unit, sequence) pairs per workgroup
-  int want = GK > 0 ? (GK + 31) / 32 : (int)(((long long)m->H * LB + 255) / 256);
+  // with several sequences every workgroup's rows serve each of them: widen
+  // by the sequence count (up to 8)
+  int want = GK > 0 ? (GK + 31) / 32 * std::min(std::max(1, LB_seq), 8) : (int)(((long long)m->H * LB + 255) / 256);
   return std::max(1, std::min(cap, want));
 }
 
@@ -541,7 +543,7 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   a.lanes_a = alstm::lanes_for_terms(m->NZ, m->D, m->H);
   for (int l = 0; l < n_levels; ++l) a.lanes_b[l] = alstm::lanes_for_level(levels[l]);
   const int maxP = std::max(1, m->num_cu);
-  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK, n_levels * B);
+  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK, n_levels * B, B);
   size_t lds = alstm::plan_progressive(a, P);
   if (m->launch_blocks == 0)   // automatic: widen until the per-workgroup slices fit in LDS
     while (lds > alstm::kLdsCap && P < maxP) {
