@@ -157,6 +157,29 @@ def main():
                 "bytes_per_launch": bytes_launch,
                 "flops_per_launch": T * algorithmic_flops_per_timestep(G, Rg, NZ, K, Bn)}
 
+    # the exact (dense) LSTM on the same sequence, timed the same way: the
+    # baseline the progressive approximation trades accuracy against
+    me = B.approx_lstm_exact_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H)
+    he = torch.empty((T, Bn, H), device=dev)
+
+    def timed_exact(steps, warmup):
+        for _ in range(warmup):
+            B.approx_lstm_exact_run(me, x, he, stream=stream)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            B.approx_lstm_exact_run(me, x, he, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        B.approx_lstm_exact_check(me)
+        return e0.elapsed_time(e1) / steps
+
+    ms_exact = timed_exact(args.sweep_steps, 5)
+    exact = {"us_per_timestep": round(ms_exact * 1e3 / T, 4), "timesteps_per_s": round(T * Bn / (ms_exact * 1e-3), 1),
+             "weights_bytes": 4 * 4 * H * (D + H)}
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(m, wl, K, args.cpu_seconds)
@@ -170,7 +193,8 @@ def main():
                                f"{int(args.prune * 100)}% pruning (NZ={NZ}), K={K}",
                    "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
         "us_per_timestep": round(us_per_ts, 4), "prepare_s": round(prep_s, 2),
-        "phases": phases, "sweep": sweep, "tune": tune, "roofline": roofline, "cpu_baseline": cpu,
+        "phases": phases, "sweep": sweep, "tune": tune, "exact_baseline": exact, "roofline": roofline,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 

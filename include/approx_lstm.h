@@ -251,6 +251,38 @@ approx_lstm_status approx_lstm_get_factors(const approx_lstm_model* m, int32_t g
 approx_lstm_status approx_lstm_get_factors_f64(const approx_lstm_model* m, int32_t group,
                                                double* sigma, double* u, double* v_unpruned);
 
+/*
+ * Exact (dense) LSTM -- the baseline the progressive approximation is
+ * measured against: gate pre-activations W_x x_t + W_h h_{t-1} + b with the
+ * full weight matrices (Sec. II, Fig. 1; the faithful LSTM of the paper's
+ * comparisons, Sec. VI-B), then the same cell update.  fp32.
+ *
+ * approx_lstm_exact_prepare -- copy the weights to the current device.
+ *   w_ih host [4H][D], w_hh host [4H][H], bias host [4H] or NULL (zeros);
+ *   gate rows i, f, g, o.  Synchronises hip_stream.
+ * approx_lstm_exact_run -- the recurrence over x device [T][B][D] (T >= 0,
+ *   B >= 1; T <= 65534) from h0, c0 device [B][H] or NULL (zeros); writes
+ *   h_out device [T][B][H] and, if not NULL, c_out device [B][H].
+ *   Asynchronous on hip_stream (allocates workspace on first use, blocking).
+ *   Bounded device waits as for approx_lstm_run (see approx_lstm_exact_check).
+ * approx_lstm_exact_check -- synchronise hip_stream and report an expired
+ *   device wait (APPROX_LSTM_ERR_DEVICE); clears the flag.
+ * approx_lstm_exact_set_launch -- workgroups of the recurrence kernel from
+ *   the next run on (0 = automatic: one per 8 hidden units, at most the
+ *   device's compute units); results do not depend on it.
+ */
+typedef struct approx_lstm_exact approx_lstm_exact;   /* opaque */
+
+approx_lstm_status approx_lstm_exact_prepare(const float* w_ih, const float* w_hh, const float* bias,
+                                             int32_t input_size, int32_t hidden_size, void* hip_stream,
+                                             approx_lstm_exact** out);
+approx_lstm_status approx_lstm_exact_run(approx_lstm_exact* m, const float* x, int32_t T, int32_t B,
+                                         const float* h0, const float* c0, float* h_out, float* c_out,
+                                         void* hip_stream);
+approx_lstm_status approx_lstm_exact_check(approx_lstm_exact* m, void* hip_stream);
+approx_lstm_status approx_lstm_exact_set_launch(approx_lstm_exact* m, int32_t blocks);
+void approx_lstm_exact_destroy(approx_lstm_exact* m);
+
 /* approx_lstm_destroy -- free the model and its device memory (NULL is a no-op). */
 void approx_lstm_destroy(approx_lstm_model* m);
 

@@ -67,12 +67,18 @@ _sigs = {
     "approx_lstm_get_timing": [_vp, _vp, _vp, _i32],
     "approx_lstm_get_factors": [_vp, _i32, _vp, _vp, _vp, _vp],
     "approx_lstm_get_factors_f64": [_vp, _i32, _vp, _vp, _vp],
+    "approx_lstm_exact_prepare": [_vp, _vp, _vp, _i32, _i32, _vp, ctypes.POINTER(_vp)],
+    "approx_lstm_exact_run": [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp],
+    "approx_lstm_exact_check": [_vp, _vp],
+    "approx_lstm_exact_set_launch": [_vp, _i32],
 }
 for _name, _args in _sigs.items():
     getattr(lib, _name).argtypes = _args
     getattr(lib, _name).restype = ctypes.c_int
 lib.approx_lstm_destroy.argtypes = [_vp]
 lib.approx_lstm_destroy.restype = None
+lib.approx_lstm_exact_destroy.argtypes = [_vp]
+lib.approx_lstm_exact_destroy.restype = None
 lib.approx_lstm_last_error.argtypes = []
 lib.approx_lstm_last_error.restype = ctypes.c_char_p
 
@@ -240,3 +246,49 @@ def approx_lstm_get_factors_f64(model, group):
 
 def approx_lstm_last_error():
     return lib.approx_lstm_last_error().decode()
+
+
+class ExactModel:
+    """Owning handle of an approx_lstm_exact (the dense baseline)."""
+
+    def __init__(self, handle, hidden_size):
+        self.handle = handle
+        self.hidden_size = hidden_size
+
+    def __del__(self, _destroy=lib.approx_lstm_exact_destroy):
+        h, self.handle = getattr(self, "handle", None), None
+        if h:
+            _destroy(h)
+
+
+def approx_lstm_exact_prepare(w_ih, w_hh, bias, input_size, hidden_size, stream=0):
+    """Host float32 weights in (gate rows i, f, g, o); returns an ExactModel."""
+    H, D = hidden_size, input_size
+    w_ih, p_ih = _host(w_ih, np.float32)
+    w_hh, p_hh = _host(w_hh, np.float32)
+    assert w_ih.shape == (4 * H, D) and w_hh.shape == (4 * H, H)
+    p_b = None
+    if bias is not None:
+        bias, p_b = _host(bias, np.float32)
+        assert bias.shape == (4 * H,)
+    out = ctypes.c_void_p()
+    _check(lib.approx_lstm_exact_prepare(p_ih, p_hh, p_b, D, H, ctypes.c_void_p(stream or 0), ctypes.byref(out)))
+    return ExactModel(out.value, H)
+
+
+def approx_lstm_exact_run(model, x, h_out, h0=None, c0=None, c_out=None, stream=None):
+    """x [T, B, D], h_out [T, B, H], c_out [B, H], h0/c0 [B, H]: GPU float32 tensors."""
+    T, B, D = x.shape
+    H = model.hidden_size
+    st = lib.approx_lstm_exact_run(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)), _dev(c0, "c0", (B, H)),
+                                   _dev(h_out, "h_out", (T, B, H)), _dev(c_out, "c_out", (B, H)),
+                                   ctypes.c_void_p(_stream(stream)))
+    return _check(st)
+
+
+def approx_lstm_exact_check(model, stream=None):
+    return _check(lib.approx_lstm_exact_check(model.handle, ctypes.c_void_p(_stream(stream))))
+
+
+def approx_lstm_exact_set_launch(model, blocks):
+    return _check(lib.approx_lstm_exact_set_launch(model.handle, int(blocks)))

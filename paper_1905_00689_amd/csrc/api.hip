@@ -866,3 +866,144 @@ approx_lstm_status approx_lstm_get_factors_f64(const approx_lstm_model* m, int32
 void approx_lstm_destroy(approx_lstm_model* m) { delete m; }
 
 }  // extern "C"
+
+struct approx_lstm_exact {
+  int D = 0, H = 0;
+  int device = -1, num_cu = 0;
+  float* d_Wx = nullptr;
+  float* d_Wh = nullptr;
+  float* d_bias = nullptr;
+  float* d_px = nullptr;
+  size_t px_cap = 0;
+  unsigned long long* d_hx = nullptr;
+  size_t hx_cap = 0;
+  unsigned* d_err = nullptr;
+  unsigned seq = 0;
+  int launch_blocks = 0;
+
+  ~approx_lstm_exact() {
+    if (device < 0) return;
+    DeviceScope ds(device);
+    dfree(d_Wx);
+    dfree(d_Wh);
+    dfree(d_bias);
+    dfree(d_px);
+    dfree(d_hx);
+    dfree(d_err);
+  }
+};
+
+extern "C" {
+
+approx_lstm_status approx_lstm_exact_prepare(const float* w_ih, const float* w_hh, const float* bias,
+                                             int32_t input_size, int32_t hidden_size, void* hip_stream,
+                                             approx_lstm_exact** out) {
+  g_last_error.clear();
+  if (!w_ih || !w_hh || !out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null pointer argument");
+  if (input_size < 1 || hidden_size < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "sizes must be >= 1");
+  approx_lstm_exact* m = new (std::nothrow) approx_lstm_exact();
+  if (!m) return fail(APPROX_LSTM_ERR_OUT_OF_MEMORY, "host allocation failed");
+  m->D = input_size;
+  m->H = hidden_size;
+  const size_t R = 4 * (size_t)m->H;
+  std::vector<float> b(R, 0.0f);
+  if (bias) std::copy(bias, bias + R, b.begin());
+  hipStream_t stream = (hipStream_t)hip_stream;
+  approx_lstm_status st = APPROX_LSTM_OK;
+  auto step = [&](hipError_t e, const char* what) {
+    if (st == APPROX_LSTM_OK && e != hipSuccess) st = hip_fail(e, what);
+  };
+  step(hipGetDevice(&m->device), "hipGetDevice");
+  if (st == APPROX_LSTM_OK) {
+    hipDeviceProp_t prop;
+    step(hipGetDeviceProperties(&prop, m->device), "hipGetDeviceProperties");
+    m->num_cu = prop.multiProcessorCount;
+  }
+  auto up = [&](float*& dst, const float* src, size_t n, const char* what) {
+    step(hipMalloc(&dst, n * 4), what);
+    if (st == APPROX_LSTM_OK) step(hipMemcpyAsync(dst, src, n * 4, hipMemcpyHostToDevice, stream), what);
+  };
+  up(m->d_Wx, w_ih, R * m->D, "W_ih");
+  up(m->d_Wh, w_hh, R * m->H, "W_hh");
+  up(m->d_bias, b.data(), R, "bias");
+  step(hipMalloc(&m->d_err, 64), "hipMalloc(err)");
+  if (st == APPROX_LSTM_OK) step(hipMemsetAsync(m->d_err, 0, 64, stream), "clear(err)");
+  if (st == APPROX_LSTM_OK) step(hipStreamSynchronize(stream), "hipStreamSynchronize");
+  if (st != APPROX_LSTM_OK) {
+    delete m;
+    return st;
+  }
+  *out = m;
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_exact_run(approx_lstm_exact* m, const float* x, int32_t T, int32_t B,
+                                         const float* h0, const float* c0, float* h_out, float* c_out,
+                                         void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (T < 0 || B < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need T >= 0 and B >= 1");
+  if (T > 65534) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T = %d exceeds 65534", T);
+  if (T == 0) return APPROX_LSTM_OK;
+  if (!x || !h_out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null x or h_out");
+  DeviceScope ds(m->device);
+  if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  hipStream_t stream = (hipStream_t)hip_stream;
+  alstm::ExactArgs a{};
+  a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
+  a.Wx = m->d_Wx; a.Wh = m->d_Wh; a.bias = m->d_bias;
+  a.D = m->D; a.H = m->H; a.T = T; a.B = B;
+  a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
+  const int maxP = std::max(1, m->num_cu);
+  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : std::min(maxP, std::max(1, (m->H + 7) / 8));
+  size_t lds = alstm::plan_exact(a, P);
+  if (m->launch_blocks == 0)
+    while (lds > alstm::kLdsCap && P < maxP) {
+      P = std::min(maxP, 2 * P);
+      lds = alstm::plan_exact(a, P);
+    }
+  if (lds > alstm::kLdsCap)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "LDS need %zu bytes exceeds 160 KiB (H=%d, B=%d)", lds, m->H, B);
+  approx_lstm_status st = grow(m->d_px, m->px_cap, (size_t)T * B * 4 * m->H, stream, "hipMalloc(px)");
+  if (st != APPROX_LSTM_OK) return st;
+  if ((size_t)B * m->H > m->hx_cap) {
+    st = grow(m->d_hx, m->hx_cap, (size_t)B * m->H, stream, "hipMalloc(hx)");
+    if (st != APPROX_LSTM_OK) return st;
+    HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+    m->seq = 0;
+  }
+  m->seq = (m->seq + 1) & 0xFFFFu;
+  if (m->seq == 0) {
+    HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+    m->seq = 1;
+  }
+  a.tag_base = m->seq << 16;
+  a.px = m->d_px; a.hx = m->d_hx; a.err = m->d_err;
+  HIP_TRY(alstm::launch_exact(a, P, stream), "launch exact_lstm_kernel");
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_exact_check(approx_lstm_exact* m, void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  DeviceScope ds(m->device);
+  HIP_TRY(hipStreamSynchronize((hipStream_t)hip_stream), "hipStreamSynchronize");
+  unsigned flag = 0;
+  HIP_TRY(hipMemcpy(&flag, m->d_err, sizeof flag, hipMemcpyDeviceToHost), "read error flag");
+  if (flag) {
+    HIP_TRY(hipMemset(m->d_err, 0, sizeof flag), "clear error flag");
+    return fail(APPROX_LSTM_ERR_DEVICE, "a device-side exchange wait exceeded its spin limit");
+  }
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_exact_set_launch(approx_lstm_exact* m, int32_t blocks) {
+  g_last_error.clear();
+  if (!m || blocks < 0) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
+  m->launch_blocks = blocks;
+  return APPROX_LSTM_OK;
+}
+
+void approx_lstm_exact_destroy(approx_lstm_exact* m) { delete m; }
+
+}  // extern "C"

@@ -1,0 +1,243 @@
+// The exact LSTM on gfx950: the dense baseline the progressive approximation
+// is measured against.  Gate pre-activations y = W_x x_t + W_h h_{t-1} + b
+// with the full weight matrices (Sec. II, Fig. 1; the augmented matrix of
+// Sec. III without any factorisation), then the same cell update.
+//
+// Two launches per run.  exact_xproj_kernel computes the x part of every
+// gate row for every timestep at once (it does not depend on h).  The
+// persistent exact_lstm_kernel then runs the recurrence: workgroup j owns a
+// slice of hidden units and the four W_h rows of each, held in registers for
+// the whole sequence, so one timestep needs a single exchange between
+// workgroups (the h all-gather), where the progressive scheme needs two
+// (z, then h).
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace alstm {
+
+namespace {
+
+constexpr int kExactLanes = 16;   // lanes per W_h row
+constexpr int kExactRows = kThreads / kExactLanes;   // rows per pass (32)
+constexpr int kExactWpl = 32;     // W_h entries per lane held in registers (H <= 512)
+constexpr int kExactCols = 16;    // x columns per staging pass of the x projection
+constexpr int kExactXprojRegs = 32;   // weights per lane of the x projection held in registers (D <= 2048)
+
+}  // namespace
+
+// px[tb][o] = b[o] + W_x[o] . x[tb] for every gate row o < 4H and column
+// tb = t*B + b.  One wave per row; the workgroup stages up to `cols` x
+// columns (contiguous in x) in LDS, read by the lanes at consecutive k.  The
+// lane's first 32 weights of its row are loaded into registers before the
+// staging, so that their latency overlaps it; the staging keeps 8 16-byte
+// loads in flight per thread when x rows are 16-byte aligned.
+__global__ void __launch_bounds__(kThreads) exact_xproj_kernel(ExactArgs a, int cols) {
+  extern __shared__ __align__(16) float xs[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int o = blockIdx.x * kWaves + wave;
+  const int TB = a.T * a.B, D = a.D, R = 4 * a.H;
+  const float* w = a.Wx + (size_t)(o < R ? o : 0) * D;
+  float wv[kExactXprojRegs];
+#pragma unroll
+  for (int i = 0; i < kExactXprojRegs; ++i) wv[i] = w[min(lane + 64 * i, D - 1)];   // masked at use
+  for (int c0 = 0; c0 < TB; c0 += cols) {
+    const int cn = min(cols, TB - c0);
+    __syncthreads();
+    const float* xsrc = a.x + (size_t)c0 * D;
+    const int n = cn * D;
+    if (a.xvec) {
+      typedef float f4 __attribute__((ext_vector_type(4)));
+      const int n4 = n >> 2;
+      for (int base = 0; base < n4; base += 8 * kThreads) {
+        f4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = base + u * kThreads + (int)threadIdx.x;
+          v[u] = reinterpret_cast<const f4*>(xsrc)[i < n4 ? i : 0];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = base + u * kThreads + (int)threadIdx.x;
+          if (i < n4) reinterpret_cast<f4*>(xs)[i] = v[u];
+        }
+      }
+    } else {
+      for (int i = threadIdx.x; i < n; i += kThreads) xs[i] = xsrc[i];
+    }
+    __syncthreads();
+    if (o < R) {
+      float acc[kExactCols];
+#pragma unroll
+      for (int c = 0; c < kExactCols; ++c) acc[c] = 0.0f;
+#pragma unroll
+      for (int i = 0; i < kExactXprojRegs; ++i) {
+        const int k = lane + 64 * i;
+        if (k < D) {
+#pragma unroll
+          for (int c = 0; c < kExactCols; ++c)
+            if (c < cn) acc[c] += wv[i] * xs[c * D + k];
+        }
+      }
+      for (int k = lane + 64 * kExactXprojRegs; k < D; k += 64) {
+        const float wk = w[k];
+#pragma unroll
+        for (int c = 0; c < kExactCols; ++c)
+          if (c < cn) acc[c] += wk * xs[c * D + k];
+      }
+#pragma unroll
+      for (int c = 0; c < kExactCols; ++c) {
+        if (c < cn) {
+          const float s = wave_sum(acc[c]);
+          if (lane == 0) a.px[(size_t)(c0 + c) * R + o] = s + a.bias[o];
+        }
+      }
+    }
+  }
+}
+
+// The recurrence.  Workgroup j owns hidden units [j*RP, j*RP + rc) and the
+// gate rows q*H + r of each (q = i, f, g, o); 16 lanes per row, rows in
+// passes of 32.  Per timestep and sequence: y = px + W_h . h_{t-1} (lane
+// partial sums, fixed-order reduction), the cell update, h published as
+// tagged words, then the full h_t gathered by every workgroup.
+__global__ void __launch_bounds__(kThreads) exact_lstm_kernel(ExactArgs a) {
+  extern __shared__ __align__(16) float lds[];
+  const int P = gridDim.x, j = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int H = a.H, B = a.B, T = a.T, RP = a.rows_per, R4 = 4 * H;
+  const int r0 = j * RP;
+  const int rc = max(0, min(RP, H - r0));
+  const int outs = 4 * rc;
+  float* hs = lds;                         // [B][H]  h_{t-1}
+  float* ys = hs + (size_t)B * H;          // [B][4*RP] y of the owned rows
+  float* cs = ys + (size_t)B * 4 * RP;     // [B][RP]   c of the owned units
+  float* hown = cs + (size_t)B * RP;       // [B][RP]   new h of the owned units
+  float* pxs = hown + (size_t)B * RP;      // [T*B][4*RP] x part of the owned rows (px_lds)
+
+  const int sl = threadIdx.x % kExactLanes, ob = threadIdx.x / kExactLanes;
+  const int passes = (outs + kExactRows - 1) / kExactRows;
+  // pass 0's row entries in registers when H fits (the common case)
+  float wr[kExactWpl];
+  const bool wreg = a.wreg != 0;
+  {
+    const int ol = ob;
+    const int q = ol < outs ? ol / rc : 0, rr = ol < outs ? ol - q * rc : 0;
+    const float* wrow = a.Wh + (size_t)(q * H + r0 + rr) * H;
+#pragma unroll
+    for (int i = 0; i < kExactWpl; ++i) {
+      const int k = sl + kExactLanes * i;
+      wr[i] = (wreg && ol < outs && k < H) ? wrow[k] : 0.0f;
+    }
+  }
+  for (int i = threadIdx.x; i < B * H; i += kThreads) {
+    const int b = i / H, r = i - b * H;
+    hs[i] = a.h0 ? a.h0[(size_t)b * H + r] : 0.0f;
+  }
+  for (int i = threadIdx.x; i < B * RP; i += kThreads) {
+    const int b = i / RP, rr = i - b * RP;
+    cs[i] = (a.c0 && rr < rc) ? a.c0[(size_t)b * H + r0 + rr] : 0.0f;
+  }
+  if (a.px_lds) {
+    for (int i = threadIdx.x; i < T * B * outs; i += kThreads) {
+      const int tb = i / outs, ol = i - tb * outs;
+      const int q = ol / rc, rr = ol - q * rc;
+      pxs[tb * 4 * RP + ol] = a.px[(size_t)tb * R4 + q * H + r0 + rr];
+    }
+  }
+  __syncthreads();
+
+  const bool local = P == 1;
+  const bool publisher = wave == kWaves - 1;
+  const int gthr = kThreads - 64;
+  for (int t = 0; t < T; ++t) {
+    const unsigned tag = a.tag_base | (unsigned)(t + 1);
+    for (int b = 0; b < B; ++b) {
+      const float* h = hs + (size_t)b * H;
+      for (int ps = 0; ps < passes; ++ps) {
+        const int ol = ob + ps * kExactRows;
+        float acc = 0.0f;
+        if (ol < outs) {
+          if (wreg && ps == 0) {
+#pragma unroll
+            for (int i = 0; i < kExactWpl; ++i) acc += wr[i] * h[min(sl + kExactLanes * i, H - 1)];
+          } else {
+            const int q = ol / rc, rr = ol - q * rc;
+            const float* wrow = a.Wh + (size_t)(q * H + r0 + rr) * H;
+#pragma unroll 4
+            for (int k = sl; k < H; k += kExactLanes) acc += wrow[k] * h[k];
+          }
+        }
+        acc = group_sum<kExactLanes>(acc);
+        if (sl == 0 && ol < outs) {
+          const int q = ol / rc, rr = ol - q * rc;
+          const float px = a.px_lds ? pxs[(t * B + b) * 4 * RP + ol] : a.px[(size_t)(t * B + b) * R4 + q * H + r0 + rr];
+          ys[b * 4 * RP + ol] = acc + px;
+        }
+      }
+    }
+    lds_barrier();
+    for (int i = threadIdx.x; i < B * rc; i += kThreads) {
+      const int b = i / rc, rr = i - b * rc;
+      const float* y = ys + b * 4 * RP;
+      const float gi = sigmoid_fast(y[0 * rc + rr]);
+      const float gf = sigmoid_fast(y[1 * rc + rr]);
+      const float gg = tanh_fast(y[2 * rc + rr]);
+      const float go = sigmoid_fast(y[3 * rc + rr]);
+      const float c = gf * cs[b * RP + rr] + gi * gg;
+      const float hv = go * tanh_fast(c);
+      cs[b * RP + rr] = c;
+      hown[b * RP + rr] = hv;
+      if (local) hs[(size_t)b * H + r0 + rr] = hv;
+    }
+    lds_barrier();
+    if (publisher) {
+      for (int i = lane; i < B * rc; i += 64) {
+        const int b = i / rc, rr = i - b * rc;
+        const float hv = hown[b * RP + rr];
+        a.h_out[((size_t)t * B + b) * H + r0 + rr] = hv;
+        if (!local) publish(a.hx + (size_t)b * H + r0 + rr, hv, tag);
+      }
+    }
+    if (!local && !publisher) gather_tagged<2>(hs, nullptr, a.hx, B * H, tag, a.err, threadIdx.x, gthr);
+    lds_barrier();
+  }
+  if (a.c_out)
+    for (int i = threadIdx.x; i < B * rc; i += kThreads) {
+      const int b = i / rc, rr = i - b * rc;
+      a.c_out[(size_t)b * H + r0 + rr] = cs[b * RP + rr];
+    }
+}
+
+size_t plan_exact(ExactArgs& a, int P) {
+  a.rows_per = (a.H + P - 1) / P;
+  a.wreg = (a.H <= kExactLanes * kExactWpl) ? 1 : 0;
+  const size_t base = 4 * ((size_t)a.B * a.H + (size_t)a.B * 4 * a.rows_per + 2 * (size_t)a.B * a.rows_per);
+  const size_t pxb = 4 * (size_t)a.T * a.B * 4 * a.rows_per;
+  a.px_lds = (base + pxb <= kLdsCap) ? 1 : 0;
+  return base + (a.px_lds ? pxb : 0);
+}
+
+hipError_t launch_exact(const ExactArgs& a, int blocks, hipStream_t stream) {
+  const int TB = a.T * a.B;
+  const int cols = std::max(1, std::min(kExactCols, (int)(kLdsCap / (4 * (size_t)a.D))));
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)exact_xproj_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)kLdsCap);
+    if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute((const void*)exact_lstm_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsCap);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const size_t xl = 4 * (size_t)std::min(cols, TB) * a.D;
+  exact_xproj_kernel<<<dim3((4 * a.H + kWaves - 1) / kWaves), dim3(kThreads), xl, stream>>>(a, cols);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  ExactArgs c = a;
+  const size_t lds = plan_exact(c, blocks);
+  if (lds > kLdsCap) return hipErrorInvalidValue;
+  exact_lstm_kernel<<<dim3(blocks), dim3(kThreads), lds, stream>>>(c);
+  return hipGetLastError();
+}
+
+}  // namespace alstm

@@ -136,6 +136,37 @@ struct BatchedArgs {
   int xvec;        // 1: x rows may be read as 16-byte vectors (D % 4 == 0, x 16-byte aligned)
 };
 
+// Exact (dense) LSTM: x [T][B][D], h0, c0 [B][H] or null, h_out [T][B][H],
+// c_out [B][H] or null; Wx [4H][D], Wh [4H][H], bias [4H] (gate rows i, f,
+// g, o); px [T*B][4H] (x part plus bias, workspace); hx [B][H] tagged words.
+struct ExactArgs {
+  const float* x;
+  const float* h0;
+  const float* c0;
+  float* h_out;
+  float* c_out;
+  const float* Wx;
+  const float* Wh;
+  const float* bias;
+  float* px;
+  unsigned long long* hx;
+  unsigned* err;
+  int D, H, T, B;
+  int xvec;        // 1: x may be read as 16-byte vectors (x 16-byte aligned, D % 4 == 0)
+  int rows_per;    // hidden units per workgroup (set by plan_exact)
+  int wreg;        // 1: the first 32 rows of each workgroup keep their W_h entries in registers
+  int px_lds;      // 1: x parts of the owned rows for every timestep in LDS
+  unsigned tag_base;
+};
+
+// Fills rows_per / wreg / px_lds for P workgroups; returns the LDS bytes the
+// recurrence kernel needs (> kLdsCap: does not fit).
+size_t plan_exact(ExactArgs& a, int P);
+
+// Launches the x projection and the persistent recurrence (`blocks`
+// workgroups) on `stream`.
+hipError_t launch_exact(const ExactArgs& a, int blocks, hipStream_t stream);
+
 // Launches, on `stream`, the x-projection once and then, for every level,
 // T pairs of per-timestep kernels.  Requires Bp % 64 == 0 and every level
 // K <= Kp.

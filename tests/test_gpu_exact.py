@@ -1,0 +1,95 @@
+"""Parity of the exact (dense) LSTM path with the float64 oracle's exact LSTM.
+
+The dense baseline computes the gate pre-activations with the full weight
+matrices (Sec. II; no factorisation), so its reference is oracle.exact_lstm,
+itself pinned to torch.nn.LSTM.  Error measure and bar as for the fp32
+progressive path (1e-4).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1905_00689_amd import synth
+from paper_1905_00689_amd import binding as B
+
+from .gpu_helpers import rel_err, say
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+
+def exact_model(w):
+    return B.approx_lstm_exact_prepare(w.W[:, :w.D], w.W[:, w.D:], w.b, w.D, w.H)
+
+
+def run_exact(m, x, h0=None, c0=None, want_c=False):
+    T, Bn, _ = x.shape
+    H = m.hidden_size
+    dev = torch.device("cuda")
+    xt = torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(dev)
+    h = torch.full((T, Bn, H), float("nan"), device=dev)
+    c = torch.full((Bn, H), float("nan"), device=dev) if want_c else None
+    h0t = None if h0 is None else torch.from_numpy(np.ascontiguousarray(h0, np.float32)).to(dev)
+    c0t = None if c0 is None else torch.from_numpy(np.ascontiguousarray(c0, np.float32)).to(dev)
+    B.approx_lstm_exact_run(m, xt, h, h0t, c0t, c)
+    B.approx_lstm_exact_check(m)
+    torch.cuda.synchronize()
+    return h.cpu().numpy(), (c.cpu().numpy() if want_c else None)
+
+
+@pytest.mark.parametrize("name", ["tiny", "driving"])
+def test_exact_matches_oracle(name):
+    w = synth.named(name)
+    say("exact LSTM", name)
+    h, _ = run_exact(exact_model(w), w.x)
+    he, _ = oracle.exact_lstm(w.W, w.b, w.x)
+    e = rel_err(h, he)
+    say("  rel err", e)
+    assert e < TOL
+
+
+def test_exact_ragged_batch_state_and_launch_widths():
+    """D=50, H=37 (hidden units split unevenly), 3 sequences with initial
+    state; every launch width gives the same bits and the oracle's values."""
+    w = synth.make(50, 37, 5, 3, index=31, xkind="relu")
+    rng = np.random.default_rng(8)
+    h0 = rng.normal(size=(3, 37)).astype(np.float32)
+    c0 = rng.normal(size=(3, 37)).astype(np.float32)
+    m = exact_model(w)
+    he, ce = oracle.exact_lstm(w.W, w.b, w.x, h0, c0)
+    ref = None
+    for P in (0, 1, 3, 7, 37):
+        say("exact ragged, blocks", P)
+        B.approx_lstm_exact_set_launch(m, P)
+        h, c = run_exact(m, w.x, h0, c0, want_c=True)
+        assert rel_err(h, he) < TOL, P
+        assert np.abs(c - ce).max() < TOL * max(1.0, np.abs(ce).max()), P
+        if ref is None:
+            ref = h
+        else:
+            assert np.array_equal(h, ref), P
+
+
+def test_exact_deadline_workload_shape():
+    """The deadline workload's shapes: D=2048, H=2048, T=64, 8 sequences."""
+    w = synth.named("deadline")
+    say("exact LSTM, deadline workload shape")
+    h, _ = run_exact(exact_model(w), w.x)
+    he, _ = oracle.exact_lstm(w.W, w.b, w.x)
+    e = rel_err(h, he)
+    say("  rel err", e)
+    assert e < TOL
+
+
+def test_exact_zero_length_and_errors():
+    w = synth.named("tiny")
+    m = exact_model(w)
+    say("exact T=0 and argument errors")
+    assert B.approx_lstm_exact_run(m, torch.zeros((0, 1, 64), device="cuda"),
+                                   torch.zeros((0, 1, 32), device="cuda")) == B.OK
+    with pytest.raises(TypeError):
+        B.approx_lstm_exact_run(m, torch.zeros((2, 1, 64)), torch.zeros((2, 1, 32)))
+    st = B.lib.approx_lstm_exact_run(m.handle, None, 2, 1, None, None, None, None, None)
+    assert st == B.ERR_INVALID_ARG
