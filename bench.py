@@ -110,6 +110,7 @@ def main():
     ms = timed(K, args.steps, args.warmup)
     us_per_ts = ms * 1e3 / T
     value = T * Bn / (ms * 1e-3)
+    dist = step_distribution(torch, lambda: B.approx_lstm_run(m, x, [K], h_out, stream=stream), stream, args.steps)
 
     sweep = {"K": [], "us_per_timestep": [], "timesteps_per_s": [], "hbm_frac": []}
     for k in [int(s) for s in args.sweep.split(",") if s]:
@@ -192,11 +193,27 @@ def main():
         "config": {"workload": "driving-shaped LSTM D=2048 H=512 T=16 B=1, per-gate rank 512, "
                                f"{int(args.prune * 100)}% pruning (NZ={NZ}), K={K}",
                    "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
-        "us_per_timestep": round(us_per_ts, 4), "prepare_s": round(prep_s, 2),
+        "us_per_timestep": round(us_per_ts, 4), "step_ms": dist, "prepare_s": round(prep_s, 2),
         "phases": phases, "sweep": sweep, "tune": tune, "exact_baseline": exact, "roofline": roofline,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def step_distribution(torch, step, stream, n):
+    """Per-step times (ms) of n further steps, each between its own pair of
+    events on the launch stream: median, p99 and max (the headline value
+    comes from the bracketed total)."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record(stream)
+        step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    t = np.sort([e0.elapsed_time(e1) for e0, e1 in evs])
+    return {"steps": n, "median": round(float(np.median(t)), 5), "p99": round(float(t[min(n - 1, int(0.99 * n))]), 5),
+            "max": round(float(t[-1]), 5)}
 
 
 def mfma_flops_batched(G, D, H, T, Bp, K):
@@ -250,6 +267,7 @@ def bench_batched(args, torch):
 
     K = args.K
     ms = timed(K, args.steps, args.warmup)
+    dist = step_distribution(torch, lambda: B.approx_lstm_run(m, x, [K], h_out, stream=stream), stream, args.steps)
     sweep = {"K": [], "us_per_timestep": [], "timesteps_per_s": [], "mfma_frac": []}
     for k in [int(v) for v in args.batched_sweep.split(",") if v]:
         msk = timed(k, args.sweep_steps, 5)
@@ -276,7 +294,7 @@ def bench_batched(args, torch):
         "config": {"workload": f"batched driving-shaped LSTM D=2048 H=512 T=16 B=256, per-gate rank 512, "
                                f"{int(args.prune * 100)}% pruning (NZ={NZ}), bf16 factors, fp32 accumulation, K={K}",
                    "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
-        "us_per_timestep": round(ms * 1e3 / T, 4), "prepare_s": round(prep_s, 2),
+        "us_per_timestep": round(ms * 1e3 / T, 4), "step_ms": dist, "prepare_s": round(prep_s, 2),
         "sweep": sweep, "roofline": roofline, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -379,17 +397,39 @@ def cpu_baseline(m, wl, K, seconds):
     import oracle
     fac = exported_terms(m)
     threads = oracle_threads()
-    runs, t0 = 0, time.time()
-    while True:
-        oracle.run(fac, wl.b, wl.x, [K])
-        runs += 1
-        el = time.time() - t0
-        if el >= seconds or runs >= 10000:
-            break
-    ts = runs * wl.T * wl.B
-    return {"value": round(ts / el, 2), "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
+    def rate(fn, budget):
+        runs, t0 = 0, time.time()
+        while True:
+            fn()
+            runs += 1
+            el = time.time() - t0
+            if el >= budget or runs >= 10000:
+                return runs * wl.T * wl.B / el, runs, el
+
+    v, runs, el = rate(lambda: oracle.run(fac, wl.b, wl.x, [K]), seconds)
+    single = exact = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            single, _, _ = rate(lambda: oracle.run(fac, wl.b, wl.x, [K]), seconds / 2)
+    except Exception:
+        pass
+    exact, _, _ = rate(lambda: oracle.exact_lstm(wl.W, wl.b, wl.x), seconds / 2)
+    return {"value": round(v, 2), "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"oracle.run (float64 NumPy) over the full T={wl.T} sequence at K={K}, "
-                      f"repeated {runs} times ({el:.1f} s), on the library's exported terms"}
+                      f"repeated {runs} times ({el:.1f} s), on the library's exported terms",
+            "single_thread_value": None if single is None else round(single, 2),
+            "exact_lstm_value": round(exact, 2), "cpu_model": cpu_model()}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 if __name__ == "__main__":
