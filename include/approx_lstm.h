@@ -265,6 +265,13 @@ approx_lstm_status approx_lstm_get_factors_f64(const approx_lstm_model* m, int32
  *   h_out device [T][B][H] and, if not NULL, c_out device [B][H].
  *   Asynchronous on hip_stream (allocates workspace on first use, blocking).
  *   Bounded device waits as for approx_lstm_run (see approx_lstm_exact_check).
+ * approx_lstm_exact_run_rows -- the same recurrence stopped after `rows`
+ *   rows of every gate (0 <= rows <= H): the anytime baseline of Sec. VI-B,
+ *   whose dense products run in tiles of rows and whose output after each
+ *   tile step is the baseline's intermediate result.  A row not reached holds
+ *   the bias alone (rows = 0: every gate is its bias; rows = H: identical to
+ *   approx_lstm_exact_run, bit for bit).  Same buffers and behaviour as
+ *   approx_lstm_exact_run; rows outside [0, H] is APPROX_LSTM_ERR_INVALID_ARG.
  * approx_lstm_exact_check -- synchronise hip_stream and report an expired
  *   device wait (APPROX_LSTM_ERR_DEVICE); clears the flag.
  * approx_lstm_exact_set_launch -- workgroups of the recurrence kernel from
@@ -279,6 +286,9 @@ approx_lstm_status approx_lstm_exact_prepare(const float* w_ih, const float* w_h
 approx_lstm_status approx_lstm_exact_run(approx_lstm_exact* m, const float* x, int32_t T, int32_t B,
                                          const float* h0, const float* c0, float* h_out, float* c_out,
                                          void* hip_stream);
+approx_lstm_status approx_lstm_exact_run_rows(approx_lstm_exact* m, const float* x, int32_t T, int32_t B,
+                                              const float* h0, const float* c0, int32_t rows, float* h_out,
+                                              float* c_out, void* hip_stream);
 approx_lstm_status approx_lstm_exact_check(approx_lstm_exact* m, void* hip_stream);
 approx_lstm_status approx_lstm_exact_set_launch(approx_lstm_exact* m, int32_t blocks);
 void approx_lstm_exact_destroy(approx_lstm_exact* m);

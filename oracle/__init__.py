@@ -10,7 +10,9 @@ arithmetic.
 What it computes follows "Approximate LSTMs for Time-Constrained Inference"
 (Rizakis et al., arXiv 1905.00689):
 
-* ``lstm``        -- the exact LSTM cell and recurrence (Sec. II, Fig. 1).
+* ``lstm``        -- the exact LSTM cell and recurrence (Sec. II, Fig. 1), and
+                     the dense baseline cut after a number of rows per gate
+                     (the row-tile anytime baseline of Sec. VI-B).
 * ``factorise``   -- the hybrid residual rank-1 SVD + magnitude pruning that
                      turns each augmented gate matrix into an ordered list of
                      refinement terms (Sec. III, Eq. (1) and the residual
@@ -26,13 +28,13 @@ routines, closed forms, invariants, brute force and the paper's printed
 numbers (no function here is "parity unpinned").
 """
 
-from .lstm import sigmoid, cell_update, exact_lstm
+from .lstm import sigmoid, cell_update, exact_lstm, row_tile_lstm
 from .factorise import Factors, nz_from_ratio, top_triplet, magnitude_mask, prepare, round_bf16
 from .progressive import run, run_schedule, reconstruct, dense_pruned_v
 from .opcount import gate_ops_progressive, gate_ops_dense, table1_efficiency
 
 __all__ = [
-    "sigmoid", "cell_update", "exact_lstm",
+    "sigmoid", "cell_update", "exact_lstm", "row_tile_lstm",
     "Factors", "nz_from_ratio", "top_triplet", "magnitude_mask", "prepare", "round_bf16",
     "run", "run_schedule", "reconstruct", "dense_pruned_v",
     "gate_ops_progressive", "gate_ops_dense", "table1_efficiency",

@@ -67,3 +67,40 @@ def exact_lstm(W, b, x, h0=None, c0=None):
         h, c = cell_update(y, c)
         hs[t] = h
     return hs, c
+
+
+def row_tile_lstm(W, b, x, rows, h0=None, c0=None):
+    """The dense baseline stopped part-way through each gate's rows.
+
+    Sec. VI-B (comparison with the FPGA baseline): the faithful LSTM computes
+    each gate's matrix-vector product in tiles of T_r rows, and the paper's
+    baseline curve takes the LSTM output after every tile step.  Reading
+    taken here: after ``rows`` rows of every gate (rows = m * T_r after m tile
+    steps, the four gates advancing together as four parallel gate units),
+    a computed row holds its full pre-activation b + W[row] . [x; h] and a row
+    not reached yet holds the bias alone (so rows = 0 coincides with the
+    progressive scheme at K = 0 and rows = H with the exact LSTM).  The same
+    row budget applies at every timestep.
+
+    W: [4H, D+H]; b: [4H] or None; x: [T, B, D]; 0 <= rows <= H.
+    Returns (h_seq [T, B, H], c_T [B, H]).
+    """
+    W = np.asarray(W, dtype=np.float64)
+    x = np.asarray(x, dtype=np.float64)
+    T, B, D = x.shape
+    H = W.shape[0] // 4
+    assert W.shape == (4 * H, D + H) and 0 <= rows <= H
+    bias = np.zeros(4 * H) if b is None else np.asarray(b, dtype=np.float64)
+    h = np.zeros((B, H)) if h0 is None else np.asarray(h0, dtype=np.float64).copy()
+    c = np.zeros((B, H)) if c0 is None else np.asarray(c0, dtype=np.float64).copy()
+    hs = np.empty((T, B, H))
+    for t in range(T):
+        xt = np.concatenate([x[t], h], axis=1)          # [B, C]
+        y = np.tile(bias, (B, 1))                        # [B, 4H]
+        for q in range(4):                               # gates i, f, g, o
+            for r in range(rows):
+                o = q * H + r
+                y[:, o] += xt @ W[o]
+        h, c = cell_update(y, c)
+        hs[t] = h
+    return hs, c

@@ -69,6 +69,7 @@ _sigs = {
     "approx_lstm_get_factors_f64": [_vp, _i32, _vp, _vp, _vp],
     "approx_lstm_exact_prepare": [_vp, _vp, _vp, _i32, _i32, _vp, ctypes.POINTER(_vp)],
     "approx_lstm_exact_run": [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp],
+    "approx_lstm_exact_run_rows": [_vp, _vp, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp],
     "approx_lstm_exact_check": [_vp, _vp],
     "approx_lstm_exact_set_launch": [_vp, _i32],
 }
@@ -283,6 +284,17 @@ def approx_lstm_exact_run(model, x, h_out, h0=None, c0=None, c_out=None, stream=
     st = lib.approx_lstm_exact_run(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)), _dev(c0, "c0", (B, H)),
                                    _dev(h_out, "h_out", (T, B, H)), _dev(c_out, "c_out", (B, H)),
                                    ctypes.c_void_p(_stream(stream)))
+    return _check(st)
+
+
+def approx_lstm_exact_run_rows(model, x, rows, h_out, h0=None, c0=None, c_out=None, stream=None):
+    """The exact recurrence stopped after `rows` rows of every gate (the
+    row-tile anytime baseline); tensors as for approx_lstm_exact_run."""
+    T, B, D = x.shape
+    H = model.hidden_size
+    st = lib.approx_lstm_exact_run_rows(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)),
+                                        _dev(c0, "c0", (B, H)), int(rows), _dev(h_out, "h_out", (T, B, H)),
+                                        _dev(c_out, "c_out", (B, H)), ctypes.c_void_p(_stream(stream)))
     return _check(st)
 
 

@@ -294,6 +294,13 @@ int auto_blocks(const approx_lstm_model* m, int GK, int LB, int LB_seq) {
   // with several sequences every workgroup's rows serve each of them: widen
   // by the sequence count (up to 8)
   int want = GK > 0 ? (GK + 31) / 32 * std::min(std::max(1, LB_seq), 8) : (int)(((long long)m->H * LB + 255) / 256);
+  // wide enough that each thread of the accumulation holds its U entries in
+  // registers (4 * units per workgroup * lanes per row <= threads)
+  if (GK > 0 && m->G > 0) {
+    const int S = alstm::lanes_for_level(GK / m->G);
+    const int rows_max = std::max(1, alstm::kThreads / (4 * S));
+    want = std::max(want, (m->H + rows_max - 1) / rows_max);
+  }
   return std::max(1, std::min(cap, want));
 }
 
@@ -937,12 +944,13 @@ approx_lstm_status approx_lstm_exact_prepare(const float* w_ih, const float* w_h
   return APPROX_LSTM_OK;
 }
 
-approx_lstm_status approx_lstm_exact_run(approx_lstm_exact* m, const float* x, int32_t T, int32_t B,
-                                         const float* h0, const float* c0, float* h_out, float* c_out,
-                                         void* hip_stream) {
+approx_lstm_status approx_lstm_exact_run_rows(approx_lstm_exact* m, const float* x, int32_t T, int32_t B,
+                                              const float* h0, const float* c0, int32_t rows, float* h_out,
+                                              float* c_out, void* hip_stream) {
   g_last_error.clear();
   if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
   if (T < 0 || B < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need T >= 0 and B >= 1");
+  if (rows < 0 || rows > m->H) return fail(APPROX_LSTM_ERR_INVALID_ARG, "rows = %d not in [0, %d]", rows, m->H);
   if (T > 65534) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T = %d exceeds 65534", T);
   if (T == 0) return APPROX_LSTM_OK;
   if (!x || !h_out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null x or h_out");
@@ -952,7 +960,7 @@ approx_lstm_status approx_lstm_exact_run(approx_lstm_exact* m, const float* x, i
   alstm::ExactArgs a{};
   a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
   a.Wx = m->d_Wx; a.Wh = m->d_Wh; a.bias = m->d_bias;
-  a.D = m->D; a.H = m->H; a.T = T; a.B = B;
+  a.D = m->D; a.H = m->H; a.T = T; a.B = B; a.rows = rows;
   a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
   const int maxP = std::max(1, m->num_cu);
   int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : std::min(maxP, std::max(1, (m->H + 7) / 8));
@@ -981,6 +989,16 @@ approx_lstm_status approx_lstm_exact_run(approx_lstm_exact* m, const float* x, i
   a.px = m->d_px; a.hx = m->d_hx; a.err = m->d_err;
   HIP_TRY(alstm::launch_exact(a, P, stream), "launch exact_lstm_kernel");
   return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_exact_run(approx_lstm_exact* m, const float* x, int32_t T, int32_t B,
+                                         const float* h0, const float* c0, float* h_out, float* c_out,
+                                         void* hip_stream) {
+  if (!m) {
+    g_last_error.clear();
+    return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  }
+  return approx_lstm_exact_run_rows(m, x, T, B, h0, c0, m->H, h_out, c_out, hip_stream);
 }
 
 approx_lstm_status approx_lstm_exact_check(approx_lstm_exact* m, void* hip_stream) {

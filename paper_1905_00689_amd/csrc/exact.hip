@@ -10,6 +10,11 @@
 // the whole sequence, so one timestep needs a single exchange between
 // workgroups (the h all-gather), where the progressive scheme needs two
 // (z, then h).
+//
+// A row budget (a.rows < H) gives the paper's anytime baseline (Sec. VI-B):
+// the dense products stopped after that many rows of every gate, the rows
+// not reached holding the bias alone.  Only the computed rows are projected
+// and multiplied.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -25,8 +30,9 @@ constexpr int kExactXprojRegs = 32;   // weights per lane of the x projection he
 
 }  // namespace
 
-// px[tb][o] = b[o] + W_x[o] . x[tb] for every gate row o < 4H and column
-// tb = t*B + b.  One wave per row; the workgroup stages up to `cols` x
+// px[tb][o] = b[o] + W_x[o] . x[tb] for every computed gate row o = q*H + r
+// (r < rows) and column tb = t*B + b; the px entries of the other rows are
+// not written.  One wave per row; the workgroup stages up to `cols` x
 // columns (contiguous in x) in LDS, read by the lanes at consecutive k.  The
 // lane's first 32 weights of its row are loaded into registers before the
 // staging, so that their latency overlaps it; the staging keeps 8 16-byte
@@ -34,9 +40,12 @@ constexpr int kExactXprojRegs = 32;   // weights per lane of the x projection he
 __global__ void __launch_bounds__(kThreads) exact_xproj_kernel(ExactArgs a, int cols) {
   extern __shared__ __align__(16) float xs[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int o = blockIdx.x * kWaves + wave;
+  const int ol = blockIdx.x * kWaves + wave;     // index among the 4*rows computed rows
   const int TB = a.T * a.B, D = a.D, R = 4 * a.H;
-  const float* w = a.Wx + (size_t)(o < R ? o : 0) * D;
+  const bool live = ol < 4 * a.rows;
+  const int q = live ? ol / a.rows : 0;
+  const int o = live ? q * a.H + (ol - q * a.rows) : 0;
+  const float* w = a.Wx + (size_t)o * D;
   float wv[kExactXprojRegs];
 #pragma unroll
   for (int i = 0; i < kExactXprojRegs; ++i) wv[i] = w[min(lane + 64 * i, D - 1)];   // masked at use
@@ -65,7 +74,7 @@ __global__ void __launch_bounds__(kThreads) exact_xproj_kernel(ExactArgs a, int 
       for (int i = threadIdx.x; i < n; i += kThreads) xs[i] = xsrc[i];
     }
     __syncthreads();
-    if (o < R) {
+    if (live) {
       float acc[kExactCols];
 #pragma unroll
       for (int c = 0; c < kExactCols; ++c) acc[c] = 0.0f;
@@ -116,17 +125,20 @@ __global__ void __launch_bounds__(kThreads) exact_lstm_kernel(ExactArgs a) {
 
   const int sl = threadIdx.x % kExactLanes, ob = threadIdx.x / kExactLanes;
   const int passes = (outs + kExactRows - 1) / kExactRows;
-  // pass 0's row entries in registers when H fits (the common case)
+  const int rlive = max(0, min(rc, a.rows - r0));   // owned units whose rows are computed
+  // pass 0's row entries in registers when H fits (the common case); zero for
+  // rows not computed, so their sums are 0
   float wr[kExactWpl];
   const bool wreg = a.wreg != 0;
   {
     const int ol = ob;
     const int q = ol < outs ? ol / rc : 0, rr = ol < outs ? ol - q * rc : 0;
+    const bool live = ol < outs && rr < rlive;
     const float* wrow = a.Wh + (size_t)(q * H + r0 + rr) * H;
 #pragma unroll
     for (int i = 0; i < kExactWpl; ++i) {
       const int k = sl + kExactLanes * i;
-      wr[i] = (wreg && ol < outs && k < H) ? wrow[k] : 0.0f;
+      wr[i] = (wreg && live && k < H) ? wrow[k] : 0.0f;
     }
   }
   for (int i = threadIdx.x; i < B * H; i += kThreads) {
@@ -141,7 +153,8 @@ __global__ void __launch_bounds__(kThreads) exact_lstm_kernel(ExactArgs a) {
     for (int i = threadIdx.x; i < T * B * outs; i += kThreads) {
       const int tb = i / outs, ol = i - tb * outs;
       const int q = ol / rc, rr = ol - q * rc;
-      pxs[tb * 4 * RP + ol] = a.px[(size_t)tb * R4 + q * H + r0 + rr];
+      const int o = q * H + r0 + rr;
+      pxs[tb * 4 * RP + ol] = rr < rlive ? a.px[(size_t)tb * R4 + o] : a.bias[o];
     }
   }
   __syncthreads();
@@ -163,14 +176,18 @@ __global__ void __launch_bounds__(kThreads) exact_lstm_kernel(ExactArgs a) {
           } else {
             const int q = ol / rc, rr = ol - q * rc;
             const float* wrow = a.Wh + (size_t)(q * H + r0 + rr) * H;
+            if (rr < rlive) {
 #pragma unroll 4
-            for (int k = sl; k < H; k += kExactLanes) acc += wrow[k] * h[k];
+              for (int k = sl; k < H; k += kExactLanes) acc += wrow[k] * h[k];
+            }
           }
         }
         acc = group_sum<kExactLanes>(acc);
         if (sl == 0 && ol < outs) {
           const int q = ol / rc, rr = ol - q * rc;
-          const float px = a.px_lds ? pxs[(t * B + b) * 4 * RP + ol] : a.px[(size_t)(t * B + b) * R4 + q * H + r0 + rr];
+          const int o = q * H + r0 + rr;
+          const float px = a.px_lds ? pxs[(t * B + b) * 4 * RP + ol]
+                                    : (rr < rlive ? a.px[(size_t)(t * B + b) * R4 + o] : a.bias[o]);
           ys[b * 4 * RP + ol] = acc + px;
         }
       }
@@ -229,10 +246,12 @@ hipError_t launch_exact(const ExactArgs& a, int blocks, hipStream_t stream) {
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const size_t xl = 4 * (size_t)std::min(cols, TB) * a.D;
-  exact_xproj_kernel<<<dim3((4 * a.H + kWaves - 1) / kWaves), dim3(kThreads), xl, stream>>>(a, cols);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (a.rows > 0) {
+    const size_t xl = 4 * (size_t)std::min(cols, TB) * a.D;
+    exact_xproj_kernel<<<dim3((4 * a.rows + kWaves - 1) / kWaves), dim3(kThreads), xl, stream>>>(a, cols);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   ExactArgs c = a;
   const size_t lds = plan_exact(c, blocks);
   if (lds > kLdsCap) return hipErrorInvalidValue;

@@ -152,6 +152,7 @@ struct ExactArgs {
   unsigned long long* hx;
   unsigned* err;
   int D, H, T, B;
+  int rows;        // rows of every gate computed (0..H); later rows hold the bias alone
   int xvec;        // 1: x may be read as 16-byte vectors (x 16-byte aligned, D % 4 == 0)
   int rows_per;    // hidden units per workgroup (set by plan_exact)
   int wreg;        // 1: the first 32 rows of each workgroup keep their W_h entries in registers

@@ -355,3 +355,35 @@ def test_deadline_full_shape_reduced_rank():
             float(np.abs(hg - he).max() / np.abs(he).max()))
         assert e < TOL, dl
     assert ks == sorted(ks) and ks[-1] == 256
+
+
+# ---------------------------------------------------------- paper shape
+@pytest.fixture(scope="module")
+def paper():
+    return synth.named("paper")
+
+
+@pytest.mark.parametrize("nz", [4160, 130, 32])
+def test_paper_shape_matches_oracle(paper, nz):
+    """The paper's model shape (Sec. VI-A: D=8256, H=64, T=100) with
+    decaying-spectrum weights, at the three non-zero counts of its error
+    curves: budgets up to 128 terms per gate (twice the gate's 64 rows; the
+    pruned terms keep refining past the rank of the matrix) against the
+    oracle on the exported terms, and the first budgets against the oracle's
+    own factors."""
+    w = paper
+    say("paper shape nz", nz, ": prepare rank 128")
+    m = B.approx_lstm_prepare(w.W[:, :w.D], w.W[:, w.D:], w.b, w.D, w.H, 128, nz=nz, groups=4)
+    levels = [0, 1, 4, 16, 64, 128]
+    h, _ = run_gpu(m, w.x, levels)
+    ho, _ = oracle.run(exported_factors(m), w.b, w.x, levels)
+    for j, K in enumerate(levels):
+        e = rel_err(h[j], ho[j])
+        say("  K", K, "rel err (exported terms)", e)
+        assert e < TOL, (K, e)
+    f = oracle.prepare(w.W, w.H, 4, nz)
+    ho, _ = oracle.run(f, w.b, w.x, [1, 4])
+    for j, K in enumerate([1, 4]):
+        e = rel_err(h[1 + j], ho[j])
+        say("  K", K, "rel err (oracle factors)", e)
+        assert e < TOL, (K, e)

@@ -426,3 +426,58 @@ def test_progressive_run_equals_exact_lstm_of_the_approximate_matrix(G, nz, K):
     he, ce = oracle.exact_lstm(Wt, w.b, w.x, h0, c0)
     np.testing.assert_allclose(hs[0], he, atol=1e-13)
     np.testing.assert_allclose(cs[0], ce, atol=1e-13)
+
+
+# ------------------------------------------------------ row-tile baseline
+def _torch_lstm(W, b, x, h0, c0):
+    T, B, D = x.shape
+    H = W.shape[0] // 4
+    lstm = torch.nn.LSTM(D, H).double()
+    with torch.no_grad():
+        lstm.weight_ih_l0.copy_(torch.from_numpy(W[:, :D]))
+        lstm.weight_hh_l0.copy_(torch.from_numpy(W[:, D:]))
+        lstm.bias_ih_l0.copy_(torch.from_numpy(b))
+        lstm.bias_hh_l0.zero_()
+        out, (_, cT) = lstm(torch.from_numpy(x), (torch.from_numpy(h0)[None], torch.from_numpy(c0)[None]))
+    return out.numpy(), cT[0].numpy()
+
+
+@pytest.mark.parametrize("rows", [0, 1, 4, 8])
+def test_row_tile_baseline_is_torch_lstm_with_unreached_rows_zeroed(rows):
+    """Sec. VI-B row-tile baseline: after `rows` rows per gate, the output is
+    the LSTM whose weight rows beyond that point (in every gate block i, f,
+    g, o) are zero and whose bias is whole.  torch.nn.LSTM on the zeroed
+    weights is an independent route to the same numbers; a wrong gate block
+    or a bias dropped from an unreached row fails it."""
+    D, H, T, B = 6, 8, 5, 3
+    W, b, rng = rand_lstm(D, H, 401 + rows)
+    x = rng.normal(size=(T, B, D))
+    h0 = rng.normal(size=(B, H))
+    c0 = rng.normal(size=(B, H))
+    Wz = W.copy()
+    for q in range(4):
+        Wz[q * H + rows:(q + 1) * H] = 0.0
+    he, ce = _torch_lstm(Wz, b, x, h0, c0)
+    hs, c = oracle.row_tile_lstm(W, b, x, rows, h0, c0)
+    np.testing.assert_allclose(hs, he, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(c, ce, rtol=0, atol=1e-12)
+
+
+def test_row_tile_baseline_limits():
+    """All rows reached is the exact LSTM; no row reached leaves the bias
+    alone, whose recurrence from h0 = c0 = 0 has the closed form
+    c_t = i g (1 - f^t) / (1 - f), h_t = o tanh(c_t)."""
+    D, H, T, B = 7, 5, 6, 2
+    W, b, rng = rand_lstm(D, H, 77)
+    x = rng.normal(size=(T, B, D))
+    hs, c = oracle.row_tile_lstm(W, b, x, H)
+    he, ce = _torch_lstm(W, b, x, np.zeros((B, H)), np.zeros((B, H)))
+    np.testing.assert_allclose(hs, he, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(c, ce, rtol=0, atol=1e-12)
+    hs0, _ = oracle.row_tile_lstm(W, b, x, 0)
+    sg = lambda z: 1 / (1 + np.exp(-z))
+    i, fg, g, o = sg(b[:H]), sg(b[H:2 * H]), np.tanh(b[2 * H:3 * H]), sg(b[3 * H:])
+    for t in range(T):
+        ct = i * g * (1 - fg ** (t + 1)) / (1 - fg)
+        for bb in range(B):
+            np.testing.assert_allclose(hs0[t, bb], o * np.tanh(ct), atol=1e-14)
