@@ -36,7 +36,8 @@ constexpr int kExactXprojRegs = 32;   // weights per lane of the x projection he
 // columns (contiguous in x) in LDS, read by the lanes at consecutive k.  The
 // lane's first 32 weights of its row are loaded into registers before the
 // staging, so that their latency overlaps it; the staging keeps 8 16-byte
-// loads in flight per thread when x rows are 16-byte aligned.
+// loads in flight per thread when x rows are 16-byte aligned.  The column
+// chunks are dealt over gridDim.y workgroups per row group.
 __global__ void __launch_bounds__(kThreads) exact_xproj_kernel(ExactArgs a, int cols) {
   extern __shared__ __align__(16) float xs[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -49,7 +50,7 @@ __global__ void __launch_bounds__(kThreads) exact_xproj_kernel(ExactArgs a, int 
   float wv[kExactXprojRegs];
 #pragma unroll
   for (int i = 0; i < kExactXprojRegs; ++i) wv[i] = w[min(lane + 64 * i, D - 1)];   // masked at use
-  for (int c0 = 0; c0 < TB; c0 += cols) {
+  for (int c0 = blockIdx.y * cols; c0 < TB; c0 += gridDim.y * cols) {
     const int cn = min(cols, TB - c0);
     __syncthreads();
     const float* xsrc = a.x + (size_t)c0 * D;
@@ -248,7 +249,9 @@ hipError_t launch_exact(const ExactArgs& a, int blocks, hipStream_t stream) {
   }
   if (a.rows > 0) {
     const size_t xl = 4 * (size_t)std::min(cols, TB) * a.D;
-    exact_xproj_kernel<<<dim3((4 * a.rows + kWaves - 1) / kWaves), dim3(kThreads), xl, stream>>>(a, cols);
+    const int gx = (4 * a.rows + kWaves - 1) / kWaves;
+    const int gy = column_slices(gx, (TB + cols - 1) / cols);
+    exact_xproj_kernel<<<dim3(gx, gy), dim3(kThreads), xl, stream>>>(a, cols);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -474,7 +474,10 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
 // spread over the GPU: each wave takes one term and each workgroup stages a
 // chunk of x transposed in LDS, xt[k][c] with a padded
 // row of xrow floats, so that one entry's values for every (t, b) of the
-// chunk are adjacent.  The term's entries are read once from HBM.
+// chunk are adjacent.  The term's entries are read once from HBM.  The
+// chunks are dealt over gridDim.y workgroups per term group, so that few
+// terms with long sequences (or wide x, hence small chunks) still fill the
+// device.
 __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xchunk, int xrow) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   float* xt = reinterpret_cast<float*>(lds_raw);
@@ -509,7 +512,7 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
         ev[w][q] = 0.0f;
         ek[w][q] = 0;
       }
-  for (int cb = 0; cb < TB; cb += xchunk) {
+  for (int cb = blockIdx.y * xchunk; cb < TB; cb += gridDim.y * xchunk) {
     const int cnt = min(xchunk, TB - cb);
     __syncthreads();
     if (a.xvec && xchunk == kMaxXChunk) {
@@ -737,7 +740,9 @@ hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hip
       proj_attr = true;
     }
     const int per_block = kWaves;       // one term per wave
-    input_proj_kernel<<<dim3((a.GK + per_block - 1) / per_block), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
+    const int gx = (a.GK + per_block - 1) / per_block;
+    const int gy = column_slices(gx, (TB + xchunk - 1) / xchunk);
+    input_proj_kernel<<<dim3(gx, gy), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -82,6 +82,14 @@ int lanes_for_level(int K);
 // bulk one a flag round and one 16-byte load per 4 values.
 inline int use_bulk_h(int L, int B, int H) { return (long long)L * B * H > 2048 ? 1 : 0; }
 
+// Workgroups along the (t, b) columns of an input projection whose rows take
+// `row_groups` workgroups and whose columns come in `chunks` chunks: enough
+// for about two workgroups per compute unit, at most one per chunk.
+inline int column_slices(int row_groups, int chunks) {
+  const int want = (512 + row_groups - 1) / row_groups;
+  return want < 1 ? 1 : (want < chunks ? want : (chunks < 1 ? 1 : chunks));
+}
+
 // Fills the launch-shape fields (rows_per .. lanes_a) for P workgroups and
 // returns the LDS bytes the kernel then needs (> kLdsCap: does not fit).
 size_t plan_progressive(RunArgs& a, int P);
