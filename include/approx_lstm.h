@@ -59,6 +59,10 @@ typedef enum {
                                                        (get_factors works, run returns INVALID_ARG) */
 #define APPROX_LSTM_FLAG_KEEP_UNPRUNED  (1ull << 1) /* keep the fp64 sigma, u and unpruned v of every
                                                        term for approx_lstm_get_factors_f64 */
+#define APPROX_LSTM_FLAG_DEVICE_FACTORISE (1ull << 2) /* run the factorisation on the current HIP device
+                                                       (float64 kernels, same scheme and stop rules;
+                                                       results agree with the host factorisation up to
+                                                       rounding); not with HOST_ONLY */
 
 typedef struct approx_lstm_model approx_lstm_model;   /* opaque */
 

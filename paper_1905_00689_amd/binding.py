@@ -25,6 +25,7 @@ ERR_UNSUPPORTED = 6
 MAX_LEVELS = 16
 FLAG_HOST_ONLY = 1 << 0
 FLAG_KEEP_UNPRUNED = 1 << 1
+FLAG_DEVICE_FACTORISE = 1 << 2
 
 
 class ApproxLstmError(RuntimeError):

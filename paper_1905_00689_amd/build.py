@@ -42,7 +42,7 @@ def build(verbose=False):
     fo = os.path.join(BUILD, "factorise.o")
     _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, "factorise.cpp"), "-o", fo], verbose)
     objs.append(fo)
-    for src in ("kernels.hip", "batched.hip", "exact.hip", "api.hip"):
+    for src in ("kernels.hip", "batched.hip", "exact.hip", "factorise_device.hip", "api.hip"):
         o = os.path.join(BUILD, src.replace(".hip", ".o"))
         _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", o], verbose)
         objs.append(o)

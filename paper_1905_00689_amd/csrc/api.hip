@@ -333,6 +333,9 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
   if (nz < 1 || nz > C) return fail(APPROX_LSTM_ERR_INVALID_ARG, "nz = %d not in [1, %d]", nz, C);
   const bool host_only = (p->flags & APPROX_LSTM_FLAG_HOST_ONLY) != 0;
   const bool keep = (p->flags & APPROX_LSTM_FLAG_KEEP_UNPRUNED) != 0;
+  const bool on_device = (p->flags & APPROX_LSTM_FLAG_DEVICE_FACTORISE) != 0;
+  if (host_only && on_device)
+    return fail(APPROX_LSTM_ERR_INVALID_ARG, "DEVICE_FACTORISE and HOST_ONLY exclude each other");
 
   approx_lstm_model* m = new (std::nothrow) approx_lstm_model();
   if (!m) return fail(APPROX_LSTM_ERR_OUT_OF_MEMORY, "host allocation failed");
@@ -357,10 +360,18 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
       if (v > 0) hw = std::min<unsigned>(hw, (unsigned)v);
     }
     opt.threads = std::max(1, (int)(hw / (unsigned)G));
-    std::vector<std::thread> th;
-    for (int g = 0; g < G; ++g)
-      th.emplace_back([&, g] { alstm::factorise_group(&W[(size_t)g * Rg * C], Rg, C, N, nz, opt, gf[g]); });
-    for (auto& t : th) t.join();
+    if (on_device) {
+      std::string err;
+      if (alstm::factorise_groups_device(W.data(), G, Rg, C, N, nz, opt, gf, hip_stream, &err) < 0) {
+        delete m;
+        return fail(APPROX_LSTM_ERR_DEVICE, "device factorisation: %s", err.c_str());
+      }
+    } else {
+      std::vector<std::thread> th;
+      for (int g = 0; g < G; ++g)
+        th.emplace_back([&, g] { alstm::factorise_group(&W[(size_t)g * Rg * C], Rg, C, N, nz, opt, gf[g]); });
+      for (auto& t : th) t.join();
+    }
 
     m->sigma.assign((size_t)G * N, 0.f);
     m->u.assign((size_t)G * N * Rg, 0.f);

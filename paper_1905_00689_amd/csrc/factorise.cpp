@@ -160,6 +160,16 @@ double tri_top_eigen(const double* a, const double* b, int m, std::vector<double
 
 }  // namespace
 
+double tridiag_top(const double* a, const double* b, int m, std::vector<double>& s) {
+  return tri_top_eigen(a, b, m, s);
+}
+
+void lanczos_start(double* q, int n) {
+  start_vector(q, n);
+  const double nq = norm2(q, n);
+  for (int i = 0; i < n; ++i) q[i] /= nq;
+}
+
 double lanczos_top(const double* G, int n, double tol, int max_iter, double* y, bool* converged,
                    int* iterations, int threads) {
   const int kmax = (max_iter > 0) ? std::min(max_iter, n) : n;
@@ -239,21 +249,57 @@ void gram_exact(const std::vector<double>& R, int rows, int cols, bool left, std
 
 }  // namespace
 
-int factorise_group(const double* W, int rows, int cols, int rank, int nz,
-                    const FactoriseOptions& opt, GroupFactors& out) {
+void init_group(GroupFactors& out, int rows, int cols, int rank, int nz, bool keep_unpruned) {
   out.rows = rows;
   out.cols = cols;
   out.rank = rank;
   out.nz = nz;
   out.sigma.assign(rank, 0.0);
   out.u.assign((size_t)rank * rows, 0.0);
-  out.v.assign(opt.keep_unpruned ? (size_t)rank * cols : 0, 0.0);
+  out.v.assign(keep_unpruned ? (size_t)rank * cols : 0, 0.0);
   out.mask.resize((size_t)rank * nz);
   for (int t = 0; t < rank; ++t)
     for (int e = 0; e < nz; ++e) out.mask[(size_t)t * nz + e] = e;   // terminated-term default
   out.vals.assign((size_t)rank * nz, 0.0);
   out.eff_rank = 0;
   out.unconverged = 0;
+}
+
+void store_term(GroupFactors& out, int t, double s, std::vector<double>& uu, std::vector<double>& vv,
+                bool keep_unpruned, std::vector<int32_t>& idx) {
+  const int cols = out.cols, nz = out.nz;
+  // sign: largest-magnitude entry of v (lowest index on ties) positive
+  int kstar = 0;
+  for (int k = 1; k < cols; ++k)
+    if (std::fabs(vv[k]) > std::fabs(vv[kstar])) kstar = k;
+  if (vv[kstar] < 0) {
+    for (auto& a : uu) a = -a;
+    for (auto& a : vv) a = -a;
+  }
+  // mask: nz largest |v|, ties to the lower index, kept ascending
+  idx.resize(cols);
+  std::iota(idx.begin(), idx.end(), 0);
+  auto before = [&](int32_t a, int32_t b) {
+    double fa = std::fabs(vv[a]), fb = std::fabs(vv[b]);
+    return fa > fb || (fa == fb && a < b);
+  };
+  if (nz < cols) std::nth_element(idx.begin(), idx.begin() + (nz - 1), idx.end(), before);
+  std::sort(idx.begin(), idx.begin() + nz, before);
+  std::sort(idx.begin(), idx.begin() + nz);
+  int32_t* mk = &out.mask[(size_t)t * nz];
+  double* vl = &out.vals[(size_t)t * nz];
+  for (int e = 0; e < nz; ++e) {
+    mk[e] = idx[e];
+    vl[e] = vv[idx[e]];
+  }
+  out.sigma[t] = s;
+  std::copy(uu.begin(), uu.end(), out.u.begin() + (size_t)t * out.rows);
+  if (keep_unpruned) std::copy(vv.begin(), vv.end(), out.v.begin() + (size_t)t * cols);
+}
+
+int factorise_group(const double* W, int rows, int cols, int rank, int nz,
+                    const FactoriseOptions& opt, GroupFactors& out) {
+  init_group(out, rows, cols, rank, nz, opt.keep_unpruned);
 
   std::vector<double> R(W, W + (size_t)rows * cols);
   const bool left = rows <= cols;
@@ -287,33 +333,9 @@ int factorise_group(const double* W, int rows, int cols, int rank, int nz,
     if (t == 0) tau = opt.stop_rel * s;
     if (!(s > tau)) break;   // this and every later term stay terminated
     if (!conv) ++out.unconverged;
-
-    // sign: largest-magnitude entry of v (lowest index on ties) positive
-    int kstar = 0;
-    for (int k = 1; k < cols; ++k)
-      if (std::fabs(vv[k]) > std::fabs(vv[kstar])) kstar = k;
-    if (vv[kstar] < 0) {
-      for (auto& a : uu) a = -a;
-      for (auto& a : vv) a = -a;
-    }
-    // mask: nz largest |v|, ties to the lower index, kept ascending
-    std::iota(idx.begin(), idx.end(), 0);
-    auto before = [&](int32_t a, int32_t b) {
-      double fa = std::fabs(vv[a]), fb = std::fabs(vv[b]);
-      return fa > fb || (fa == fb && a < b);
-    };
-    if (nz < cols) std::nth_element(idx.begin(), idx.begin() + (nz - 1), idx.end(), before);
-    std::sort(idx.begin(), idx.begin() + nz, before);
-    std::sort(idx.begin(), idx.begin() + nz);
-    int32_t* mk = &out.mask[(size_t)t * nz];
-    double* vl = &out.vals[(size_t)t * nz];
-    for (int e = 0; e < nz; ++e) {
-      mk[e] = idx[e];
-      vl[e] = vv[idx[e]];
-    }
-    out.sigma[t] = s;
-    std::copy(uu.begin(), uu.end(), out.u.begin() + (size_t)t * rows);
-    if (opt.keep_unpruned) std::copy(vv.begin(), vv.end(), out.v.begin() + (size_t)t * cols);
+    store_term(out, t, s, uu, vv, opt.keep_unpruned, idx);
+    const int32_t* mk = &out.mask[(size_t)t * nz];
+    const double* vl = &out.vals[(size_t)t * nz];
 
     // Gram update for R' = R - s u v'^T (v' = v on the mask), from the pre-update R
     double vp2 = 0.0;

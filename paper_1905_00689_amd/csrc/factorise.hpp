@@ -4,6 +4,7 @@
 #pragma once
 
 #include <cstdint>
+#include <string>
 #include <vector>
 
 namespace alstm {
@@ -33,6 +34,30 @@ struct FactoriseOptions {
 // result is still complete).
 int factorise_group(const double* W, int rows, int cols, int rank, int nz,
                     const FactoriseOptions& opt, GroupFactors& out);
+
+// Pieces shared by the host and the device factorisations.
+// init_group: size `out` for `rank` terms, every term terminated (zero).
+void init_group(GroupFactors& out, int rows, int cols, int rank, int nz, bool keep_unpruned);
+// store_term: term t from its singular value s and unit vectors uu (rows) and
+// vv (cols): the sign rule (v's largest-magnitude entry, lowest index on
+// ties, made positive; uu and vv are flipped in place), the mask (the nz
+// largest |v|, ties to the lower index, stored ascending) and the values.
+void store_term(GroupFactors& out, int t, double s, std::vector<double>& uu, std::vector<double>& vv,
+                bool keep_unpruned, std::vector<int32_t>& idx);
+// tridiag_top: largest eigenvalue and unit eigenvector s of the m x m
+// symmetric tridiagonal matrix with diagonal a and off-diagonal b.
+double tridiag_top(const double* a, const double* b, int m, std::vector<double>& s);
+// lanczos_start: the fixed unit start vector of every Lanczos solve.
+void lanczos_start(double* q, int n);
+
+// Factorise the G groups of W ([G*rows][cols] row-major, float64; group g is
+// rows g*rows .. g*rows+rows-1) on the current HIP device, on hip_stream,
+// with the same scheme and options as factorise_group (threads unused).
+// Returns 0, 1 if a solve did not converge (the result is still complete),
+// or -1 on a HIP error (text in *err).  Synchronises hip_stream.
+int factorise_groups_device(const double* W, int G, int rows, int cols, int rank, int nz,
+                            const FactoriseOptions& opt, std::vector<GroupFactors>& out, void* hip_stream,
+                            std::string* err);
 
 // Top eigenpair of the symmetric n x n matrix G (row-major) by Lanczos with
 // full reorthogonalisation from a fixed pseudo-random start.  Writes the unit

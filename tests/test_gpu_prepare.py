@@ -1,0 +1,164 @@
+"""The factorisation on the GPU (APPROX_LSTM_FLAG_DEVICE_FACTORISE): the same
+greedy scheme as the host factorisation (Sec. III, Eq. (1)) in float64
+kernels.  Held to the bar of the host factorisation: the whole chain
+bit-exact in masks and order on the tiny workload, the chain prefix inside
+the agreement horizon on the driving workload, one-step parity (the oracle's
+own step from the residual the library's earlier terms leave) at steps
+across long chains, and the residual-energy identity along the chain."""
+
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1905_00689_amd import synth
+from paper_1905_00689_amd import binding as B
+from tests.onestep import check_steps
+
+from .gpu_helpers import exported_factors, rel_err, say
+
+pytestmark = pytest.mark.gpu
+DEV = B.FLAG_DEVICE_FACTORISE | B.FLAG_KEEP_UNPRUNED
+
+
+def prep(w, rank, nz=0, p=0.0, groups=4, flags=DEV):
+    D, H = w.D, w.H
+    return B.approx_lstm_prepare(w.W[:, :D], w.W[:, D:], w.b, D, H, rank, nz=nz, prune_ratio=p,
+                                 groups=groups, flags=flags)
+
+
+@pytest.mark.parametrize("G", [4, 1])
+@pytest.mark.parametrize("p", [0.0, 0.5])
+def test_tiny_chain_bit_exact_with_oracle(G, p):
+    """Tiny workload (D=64, H=32; G=4 factorises 32 x 96 blocks through
+    R R^T, G=1 the 128 x 96 stack through R^T R): the whole 96-step chain."""
+    w = synth.named("tiny")
+    say("device prepare tiny G", G, "p", p)
+    nz = oracle.nz_from_ratio(96, p)
+    m = prep(w, 96, p=p, groups=G)
+    f = oracle.prepare(w.W, 32, 96, nz, groups=G)
+    info = m.info
+    assert info["nz"] == nz and info["eff_rank"] == list(f.eff_rank)
+    assert info["unconverged_steps"] == 0 and m.status == B.OK
+    for g in range(G):
+        lf = B.approx_lstm_get_factors(m, g)
+        l64 = B.approx_lstm_get_factors_f64(m, g)
+        assert np.array_equal(lf["v_idx"], f.mask[g])
+        np.testing.assert_allclose(l64["sigma"], f.sigma[g], rtol=1e-11, atol=1e-14)
+        np.testing.assert_allclose(l64["u"], f.U[g], atol=1e-9)
+        np.testing.assert_allclose(l64["v"], f.v_full[g], atol=1e-9)
+        assert np.array_equal(lf["sigma"], l64["sigma"].astype(np.float32))
+        assert np.array_equal(lf["u"], l64["u"].astype(np.float32))
+
+
+def test_tiny_device_model_runs_like_the_oracle():
+    w = synth.named("tiny")
+    say("device prepare tiny: run parity")
+    m = prep(w, 48, p=0.5)
+    f = exported_factors(m)
+    x = torch.from_numpy(w.x).cuda()
+    h = torch.full((3, w.T, 1, w.H), float("nan"), device="cuda")
+    B.approx_lstm_run(m, x, [1, 12, 48], h)
+    B.approx_lstm_check(m)
+    ho, _ = oracle.run(f, w.b, w.x, [1, 12, 48])
+    assert rel_err(h.cpu().numpy(), ho) < 1e-4
+
+
+@pytest.fixture(scope="module")
+def driving():
+    return synth.named("driving")
+
+
+def test_driving_chain_prefix_bit_exact(driving):
+    """Driving workload, 75% pruning: the first 24 steps of every gate match
+    the oracle's chain in masks and order."""
+    say("device prepare driving p=0.75, 24 steps")
+    nz = oracle.nz_from_ratio(2560, 0.75)
+    m = prep(driving, 24, p=0.75)
+    f = oracle.prepare(driving.W, 512, 24, nz)
+    for g in range(4):
+        lf = B.approx_lstm_get_factors(m, g)
+        assert np.array_equal(lf["v_idx"], f.mask[g]), g
+        l64 = B.approx_lstm_get_factors_f64(m, g)
+        np.testing.assert_allclose(l64["sigma"], f.sigma[g], rtol=1e-7)
+
+
+def test_driving_full_chain_one_step_parity_and_certificates(driving):
+    """Rank 512 at 75% pruning (the timed workload): one-step parity at steps
+    across the chain, and ||R^(n)||_F^2 from the terms equal to the
+    accumulated sum ||W||^2 - sum sigma^2 ||v'||^2."""
+    say("device prepare driving p=0.75 rank 512")
+    t0 = time.time()
+    m = prep(driving, 512, p=0.75)
+    say("  prepare s", round(time.time() - t0, 2))
+    assert m.info["eff_rank"] == [512] * 4 and m.info["unconverged_steps"] == 0
+    W = driving.W.astype(np.float64)
+    steps = [0, 1, 2, 63, 64, 127, 255, 300, 447, 511]
+    for g in (0, 2):
+        Wg = W[g * 512:(g + 1) * 512]
+        lf = B.approx_lstm_get_factors(m, g)
+        l64 = B.approx_lstm_get_factors_f64(m, g)
+        idx = lf["v_idx"].astype(np.int64)
+        res = check_steps(Wg, l64["sigma"], l64["u"], l64["v"], idx, 640, steps)
+        assert all(s == "exact" for _, s in res), res
+        vp = np.take_along_axis(l64["v"], idx, axis=1)
+        R = Wg.copy()
+        e0 = acc = np.sum(Wg * Wg)
+        for n in range(512):
+            R[:, idx[n]] -= l64["sigma"][n] * np.outer(l64["u"][n], vp[n])
+            acc -= l64["sigma"][n] ** 2 * np.sum(vp[n] ** 2)
+            if n in (0, 100, 511):
+                assert abs(np.sum(R * R) - acc) <= 1e-9 * e0, (g, n)
+
+
+def test_device_and_host_factorisations_agree_on_the_prefix(driving):
+    say("device vs host prepare, driving p=0.9, 16 steps")
+    md = prep(driving, 16, p=0.9)
+    mh = prep(driving, 16, p=0.9, flags=B.FLAG_HOST_ONLY | B.FLAG_KEEP_UNPRUNED)
+    for g in range(4):
+        a, b = B.approx_lstm_get_factors_f64(md, g), B.approx_lstm_get_factors_f64(mh, g)
+        assert np.array_equal(B.approx_lstm_get_factors(md, g)["v_idx"], B.approx_lstm_get_factors(mh, g)["v_idx"])
+        np.testing.assert_allclose(a["sigma"], b["sigma"], rtol=1e-9)
+
+
+def test_device_prepare_rejects_host_only():
+    w = synth.named("tiny")
+    with pytest.raises(B.ApproxLstmError) as ei:
+        prep(w, 4, p=0.5, flags=B.FLAG_DEVICE_FACTORISE | B.FLAG_HOST_ONLY)
+    assert ei.value.status == B.ERR_INVALID_ARG
+
+
+def test_deadline_workload_full_rank_on_device():
+    """The deadline workload at its full size (D=2048, H=2048, 90% pruning,
+    rank 2048 per gate), factorised on the device: one-step parity at steps
+    across the chain of one gate, then a run at three budgets against the
+    oracle on the exported terms (T=64, 8 sequences)."""
+    w = synth.named("deadline")
+    say("device prepare deadline rank 2048 p=0.9")
+    t0 = time.time()
+    m = prep(w, 2048, p=0.9)
+    say("  prepare s", round(time.time() - t0, 2))
+    inf = m.info
+    assert inf["unconverged_steps"] == 0 and min(inf["eff_rank"]) == 2048
+    W = w.W.astype(np.float64)
+    g = 1
+    lf = B.approx_lstm_get_factors(m, g)
+    l64 = B.approx_lstm_get_factors_f64(m, g)
+    say("  one-step parity, gate", g)
+    res = check_steps(W[g * 2048:(g + 1) * 2048], l64["sigma"], l64["u"], l64["v"],
+                      lf["v_idx"].astype(np.int64), inf["nz"], [0, 1, 511, 1024, 2047])
+    assert all(s == "exact" for _, s in res), res
+    say("  run vs oracle on exported terms")
+    levels = [1, 256, 2048]
+    x = torch.from_numpy(w.x).cuda()
+    h = torch.full((3, w.T, w.B, w.H), float("nan"), device="cuda")
+    B.approx_lstm_run(m, x, levels, h)
+    B.approx_lstm_check(m)
+    ho, _ = oracle.run(exported_factors(m), w.b, w.x, levels)
+    hg = h.cpu().numpy()
+    for j, K in enumerate(levels):
+        e = rel_err(hg[j], ho[j])
+        say("  K", K, "rel err", e)
+        assert e < 1e-4, (K, e)
