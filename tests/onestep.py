@@ -17,10 +17,11 @@ def residual_before(Wg, sig, U, V, masks, n):
     return R
 
 
-def check_steps(Wg, sig, U, V, masks, nz, steps, gap_floor=1e-9):
+def check_steps(Wg, sig, U, V, masks, nz, steps, gap_floor=1e-9, progress=None):
     """Returns a list of (n, status) with status 'exact' (masks equal) or
     'tie' (mask threshold gap below gap_floor, either mask acceptable).
-    Raises AssertionError on a real disagreement."""
+    Raises AssertionError on a real disagreement.  progress(n), if given, is
+    called after each checked step."""
     out = []
     steps = sorted(steps)
     R = np.array(Wg, dtype=np.float64, copy=True)
@@ -43,4 +44,6 @@ def check_steps(Wg, sig, U, V, masks, nz, steps, gap_floor=1e-9):
             gap = (a[nz - 1] - a[nz]) / a[nz - 1] if nz < len(a) else 1.0
             assert gap < gap_floor, (n, gap)
             out.append((n, "tie"))
+        if progress:
+            progress(n)
     return out

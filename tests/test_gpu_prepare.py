@@ -133,7 +133,7 @@ def test_device_prepare_rejects_host_only():
 def test_deadline_workload_full_rank_on_device():
     """The deadline workload at its full size (D=2048, H=2048, 90% pruning,
     rank 2048 per gate), factorised on the device: one-step parity at steps
-    across the chain of one gate, then a run at three budgets against the
+    across the chain of one gate, then runs at K = 1 and 2048 against the
     oracle on the exported terms (T=64, 8 sequences)."""
     w = synth.named("deadline")
     say("device prepare deadline rank 2048 p=0.9")
@@ -148,17 +148,19 @@ def test_deadline_workload_full_rank_on_device():
     l64 = B.approx_lstm_get_factors_f64(m, g)
     say("  one-step parity, gate", g)
     res = check_steps(W[g * 2048:(g + 1) * 2048], l64["sigma"], l64["u"], l64["v"],
-                      lf["v_idx"].astype(np.int64), inf["nz"], [0, 1, 511, 1024, 2047])
+                      lf["v_idx"].astype(np.int64), inf["nz"], [0, 1024, 2047],
+                      progress=lambda n: say("    step", n, "checked"))
     assert all(s == "exact" for _, s in res), res
-    say("  run vs oracle on exported terms")
-    levels = [1, 256, 2048]
+    # one level per run: at H = 2048 with 8 sequences the recurrence's LDS
+    # holds the h of one level only
+    f = exported_factors(m)
     x = torch.from_numpy(w.x).cuda()
-    h = torch.full((3, w.T, w.B, w.H), float("nan"), device="cuda")
-    B.approx_lstm_run(m, x, levels, h)
-    B.approx_lstm_check(m)
-    ho, _ = oracle.run(exported_factors(m), w.b, w.x, levels)
-    hg = h.cpu().numpy()
-    for j, K in enumerate(levels):
-        e = rel_err(hg[j], ho[j])
+    h = torch.full((1, w.T, w.B, w.H), float("nan"), device="cuda")
+    for K in (1, 2048):
+        say("  run K", K, "vs oracle on exported terms")
+        B.approx_lstm_run(m, x, [K], h)
+        B.approx_lstm_check(m)
+        ho, _ = oracle.run(f, w.b, w.x, [K])
+        e = rel_err(h.cpu().numpy()[0], ho[0])
         say("  K", K, "rel err", e)
         assert e < 1e-4, (K, e)
