@@ -273,8 +273,11 @@ def anytime_curves(torch, B, wl, stream, configs, Ks, rows_list, steps=30):
 
     prog = {}
     hk = torch.empty((1, T, Bn, H), device=dev)
-    for rank, nz in configs:
-        m = B.approx_lstm_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H, rank, nz=nz, groups=4)
+    for cfg in configs:
+        rank, nz = cfg[0], cfg[1]
+        residual = len(cfg) < 3 or cfg[2] != "non-residual"
+        flags = 0 if residual else B.FLAG_NON_RESIDUAL
+        m = B.approx_lstm_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H, rank, nz=nz, groups=4, flags=flags)
         c = {"nz": m.info["nz"], "rank": rank, "K": [], "us_per_timestep": [], "rel_err": [], "kl": []}
         for k in Ks:
             if k > rank:
@@ -286,7 +289,7 @@ def anytime_curves(torch, B, wl, stream, configs, Ks, rows_list, steps=30):
             c["us_per_timestep"].append(round(us, 3))
             c["rel_err"].append(_sig(e))
             c["kl"].append(_sig(kl))
-        prog[str(c["nz"])] = c
+        prog[str(c["nz"]) + ("" if residual else "-nonres")] = c
         del m
 
     def fastest(us, err, level):
@@ -297,7 +300,8 @@ def anytime_curves(torch, B, wl, stream, configs, Ks, rows_list, steps=30):
     for level in [1e-2, 1e-3, 1e-4, 1e-5, 1e-6]:
         row = {"kl": level, "row_tile_us": fastest(tiles["us_per_timestep"], tiles["kl"], level)}
         for name, c in prog.items():
-            row["nz" + name + "_us"] = fastest(c["us_per_timestep"], c["kl"], level)
+            if not name.endswith("-nonres"):
+                row["nz" + name + "_us"] = fastest(c["us_per_timestep"], c["kl"], level)
         best = [v for k, v in row.items() if k.startswith("nz") and v is not None]
         row["speedup"] = round(row["row_tile_us"] / min(best), 3) if best and row["row_tile_us"] else None
         tte.append(row)
@@ -320,8 +324,11 @@ def anytime_comparison(torch, B, stream):
         out[name] = anytime_curves(torch, B, synth.named(name), stream, [(512, 640)], Kd, rows_d)
     Kp = [0, 1, 2, 4, 8, 16, 24, 32, 48, 64, 96, 128]
     rows_p = [0, 4, 8, 16, 24, 32, 40, 48, 56, 60, 62, 63, 64]
-    out["paper"] = anytime_curves(torch, B, synth.named("paper"), stream, [(128, 4160), (128, 130), (128, 32)],
-                                  Kp, rows_p)
+    # the non-residual alternative of Sec. III at NZ = 130 and 4160: same
+    # cost per step, larger error at every budget
+    out["paper"] = anytime_curves(torch, B, synth.named("paper"), stream,
+                                  [(128, 4160), (128, 130), (128, 32), (64, 4160, "non-residual"),
+                                   (64, 130, "non-residual")], Kp, rows_p)
     return out
 
 

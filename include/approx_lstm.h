@@ -63,6 +63,11 @@ typedef enum {
                                                        (float64 kernels, same scheme and stop rules;
                                                        results agree with the host factorisation up to
                                                        rounding); not with HOST_ONLY */
+#define APPROX_LSTM_FLAG_NON_RESIDUAL   (1ull << 3) /* ablation (Sec. III): deflate each term with its
+                                                       whole v, so that the terms are the singular
+                                                       triplets of the original gate matrix, each v
+                                                       pruned on its own and the pruning error never
+                                                       corrected by a later term */
 
 typedef struct approx_lstm_model approx_lstm_model;   /* opaque */
 

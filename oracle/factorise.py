@@ -141,13 +141,19 @@ class Factors:
                        list(self.trajectory))
 
 
-def prepare(W, H, rank, nz, groups=4, record_trajectory=False):
+def prepare(W, H, rank, nz, groups=4, record_trajectory=False, residual=True):
     """Factorise W = [W_ih | W_hh] ([4H, D+H], gate rows i, f, g, o) into
     ``rank`` pruned rank-1 refinement terms per group (Eq. (1)).
 
     For each group: R <- W_g; for n = 1..rank take the top triplet of R, fix
     its sign, keep the NZ largest-magnitude entries of v, store the term, and
     subtract sigma * u * prune(v)^T from R (the residual R^(n+1) = W - W~^(n)).
+
+    residual=False is the alternative Sec. III contrasts the scheme with:
+    successive higher-rank approximations of the original matrix, each term
+    pruned on its own.  R then loses sigma * u * v^T with the unpruned v, so
+    the terms are the singular triplets of W_g in order and the error that
+    pruning leaves is never corrected by a later term.
     """
     W = np.asarray(W, dtype=np.float64)
     fourH, C = W.shape
@@ -180,7 +186,10 @@ def prepare(W, H, rank, nz, groups=4, record_trajectory=False):
             mask[g, n] = m
             vals[g, n] = v[m]
             vfull[g, n] = v
-            R[:, m] -= s * np.outer(u, v[m])
+            if residual:
+                R[:, m] -= s * np.outer(u, v[m])
+            else:
+                R -= s * np.outer(u, v)
             live = n + 1
             if record_trajectory:
                 tr.append(float(np.sum(R * R)))

@@ -26,6 +26,7 @@ MAX_LEVELS = 16
 FLAG_HOST_ONLY = 1 << 0
 FLAG_KEEP_UNPRUNED = 1 << 1
 FLAG_DEVICE_FACTORISE = 1 << 2
+FLAG_NON_RESIDUAL = 1 << 3
 
 
 class ApproxLstmError(RuntimeError):

@@ -352,6 +352,7 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
     }
     alstm::FactoriseOptions opt;
     opt.keep_unpruned = keep;
+    opt.residual = (p->flags & APPROX_LSTM_FLAG_NON_RESIDUAL) == 0;
     // groups run on their own threads; the host's thread budget (OMP_NUM_THREADS
     // when set, else the hardware's) is split over the row loops of the groups
     unsigned hw = std::max(1u, std::thread::hardware_concurrency());

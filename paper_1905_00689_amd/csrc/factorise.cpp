@@ -308,7 +308,8 @@ int factorise_group(const double* W, int rows, int cols, int rank, int nz,
   gram_exact(R, rows, cols, left, G, opt.threads);
 
   std::vector<double> y(n), uu(rows), vv(cols), w(left ? rows : cols);
-  std::vector<int32_t> idx(cols);
+  std::vector<int32_t> idx(cols), all_cols(cols);
+  std::iota(all_cols.begin(), all_cols.end(), 0);
   double tau = 0.0;
   for (int t = 0; t < rank; ++t) {
     if (t > 0 && opt.gram_refresh > 0 && t % opt.gram_refresh == 0) gram_exact(R, rows, cols, left, G, opt.threads);
@@ -334,17 +335,21 @@ int factorise_group(const double* W, int rows, int cols, int rank, int nz,
     if (!(s > tau)) break;   // this and every later term stay terminated
     if (!conv) ++out.unconverged;
     store_term(out, t, s, uu, vv, opt.keep_unpruned, idx);
-    const int32_t* mk = &out.mask[(size_t)t * nz];
-    const double* vl = &out.vals[(size_t)t * nz];
+    // the factor the residual loses: sigma u v'^T with the pruned v' (the
+    // residual scheme), or sigma u v^T with the whole v (the alternative of
+    // successive approximations of the original matrix)
+    const int nzu = opt.residual ? nz : cols;
+    const int32_t* mk = opt.residual ? &out.mask[(size_t)t * nz] : all_cols.data();
+    const double* vl = opt.residual ? &out.vals[(size_t)t * nz] : vv.data();
 
-    // Gram update for R' = R - s u v'^T (v' = v on the mask), from the pre-update R
+    // Gram update for R' = R - s u v'^T, from the pre-update R
     double vp2 = 0.0;
-    for (int e = 0; e < nz; ++e) vp2 += vl[e] * vl[e];
+    for (int e = 0; e < nzu; ++e) vp2 += vl[e] * vl[e];
     if (left) {
       for (int r = 0; r < rows; ++r) {   // w = R v'
         const double* rr = &R[(size_t)r * cols];
         double acc = 0.0;
-        for (int e = 0; e < nz; ++e) acc += rr[mk[e]] * vl[e];
+        for (int e = 0; e < nzu; ++e) acc += rr[mk[e]] * vl[e];
         w[r] = acc;
       }
       for (int i = 0; i < rows; ++i) {
@@ -356,21 +361,21 @@ int factorise_group(const double* W, int rows, int cols, int rank, int nz,
       for (int k = 0; k < cols; ++k) w[k] = 0.0;   // p = R^T u
       for (int r = 0; r < rows; ++r) axpy(uu[r], &R[(size_t)r * cols], w.data(), cols);
       double usq = dot(uu.data(), uu.data(), rows);
-      for (int e = 0; e < nz; ++e) {
+      for (int e = 0; e < nzu; ++e) {
         const int i = mk[e];
         const double vi = vl[e];
         double* gi = &G[(size_t)i * cols];
         for (int j = 0; j < cols; ++j) gi[j] -= s * vi * w[j];
         for (int j = 0; j < cols; ++j) G[(size_t)j * cols + i] -= s * w[j] * vi;
       }
-      for (int e = 0; e < nz; ++e)
-        for (int f = 0; f < nz; ++f) G[(size_t)mk[e] * cols + mk[f]] += s * s * usq * vl[e] * vl[f];
+      for (int e = 0; e < nzu; ++e)
+        for (int f = 0; f < nzu; ++f) G[(size_t)mk[e] * cols + mk[f]] += s * s * usq * vl[e] * vl[f];
     }
     // residual update
     for (int r = 0; r < rows; ++r) {
       double* rr = &R[(size_t)r * cols];
       const double a = s * uu[r];
-      for (int e = 0; e < nz; ++e) rr[mk[e]] -= a * vl[e];
+      for (int e = 0; e < nzu; ++e) rr[mk[e]] -= a * vl[e];
     }
     out.eff_rank = t + 1;
   }

@@ -27,6 +27,8 @@ struct FactoriseOptions {
   double lanczos_tol = 4e-14;   // Ritz residual / Ritz value at which a solve stops
   double stop_rel = 1e-12;      // sigma <= stop_rel * sigma_1 ends the term list
   int max_lanczos = 0;          // 0: up to the Gram size
+  bool residual = true;         // false: each term is deflated with its whole v (successive
+                                // approximations of the original matrix), not its pruned v
 };
 
 // Factorise W (rows x cols, row-major, float64) into `rank` terms keeping

@@ -562,13 +562,19 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
       if (!conv[g]) ++out[g].unconverged;
       store_term(out[g], t, sg, uu, vv, opt.keep_unpruned, idx);
       out[g].eff_rank = t + 1;
-      // pruned v' as a dense vector (zeros off the mask)
+      // the v the residual loses: pruned v' as a dense vector (zeros off the
+      // mask), or the whole v for the non-residual alternative
       std::vector<double> vp(cols, 0.0);
       double vp2 = 0.0;
-      for (int e = 0; e < nz; ++e) {
-        const double val = out[g].vals[(size_t)t * nz + e];
-        vp[out[g].mask[(size_t)t * nz + e]] = val;
-        vp2 += val * val;
+      if (opt.residual) {
+        for (int e = 0; e < nz; ++e) {
+          const double val = out[g].vals[(size_t)t * nz + e];
+          vp[out[g].mask[(size_t)t * nz + e]] = val;
+          vp2 += val * val;
+        }
+      } else {
+        vp = vv;
+        for (double a : vp) vp2 += a * a;
       }
       double* ag = &ha[(size_t)g * n];
       double* bg = &hb[(size_t)g * m];

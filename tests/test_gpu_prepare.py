@@ -164,3 +164,22 @@ def test_deadline_workload_full_rank_on_device():
         e = rel_err(h.cpu().numpy()[0], ho[0])
         say("  K", K, "rel err", e)
         assert e < 1e-4, (K, e)
+
+
+@pytest.mark.parametrize("G", [4, 1])
+def test_non_residual_ablation_on_device_matches_oracle(G):
+    """APPROX_LSTM_FLAG_NON_RESIDUAL with the device factorisation: the
+    terms are the pruned singular triplets of the original matrix, as the
+    oracle's residual=False computes them."""
+    w = synth.named("tiny")
+    say("device prepare tiny non-residual G", G)
+    nz = oracle.nz_from_ratio(96, 0.5)
+    rank = 32 if G == 4 else 96
+    m = prep(w, rank, p=0.5, groups=G, flags=DEV | B.FLAG_NON_RESIDUAL)
+    f = oracle.prepare(w.W, 32, rank, nz, groups=G, residual=False)
+    assert m.info["eff_rank"] == list(f.eff_rank)
+    for g in range(G):
+        lf = B.approx_lstm_get_factors(m, g)
+        l64 = B.approx_lstm_get_factors_f64(m, g)
+        assert np.array_equal(lf["v_idx"], f.mask[g])
+        np.testing.assert_allclose(l64["sigma"], f.sigma[g], rtol=1e-11, atol=1e-14)

@@ -212,3 +212,32 @@ def test_too_wide_input_is_unsupported():
         B.approx_lstm_prepare(np.zeros((32, D), np.float32), np.zeros((32, H), np.float32), None,
                               D, H, 1, nz=1, flags=HOST)
     assert ei.value.status == B.ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("G", [4, 1])
+def test_non_residual_ablation_matches_oracle(G):
+    """APPROX_LSTM_FLAG_NON_RESIDUAL (Sec. III's alternative): the library's
+    terms equal the oracle's residual=False terms, masks bit-exact over the
+    tiny workload's chain (up to the rank of the gate matrix, where the
+    spectrum ends)."""
+    w = synth.named("tiny")
+    nz = oracle.nz_from_ratio(96, 0.5)
+    rank = 32 if G == 4 else 96
+    m = prep(w, rank, p=0.5, groups=G, flags=HOST | B.FLAG_NON_RESIDUAL)
+    f = oracle.prepare(w.W, 32, rank, nz, groups=G, residual=False)
+    assert m.info["eff_rank"] == list(f.eff_rank)
+    for g in range(G):
+        lf = B.approx_lstm_get_factors(m, g)
+        l64 = B.approx_lstm_get_factors_f64(m, g)
+        assert np.array_equal(lf["v_idx"], f.mask[g])
+        np.testing.assert_allclose(l64["sigma"], f.sigma[g], rtol=1e-11, atol=1e-14)
+        np.testing.assert_allclose(l64["v"], f.v_full[g], atol=1e-9)
+
+
+def test_non_residual_driving_prefix():
+    w = synth.named("driving")
+    nz = oracle.nz_from_ratio(2560, 0.75)
+    m = prep(w, 24, p=0.75, flags=HOST | B.FLAG_NON_RESIDUAL)
+    f = oracle.prepare(w.W, 512, 24, nz, residual=False)
+    for g in range(4):
+        assert np.array_equal(B.approx_lstm_get_factors(m, g)["v_idx"], f.mask[g]), g

@@ -481,3 +481,46 @@ def test_row_tile_baseline_limits():
         ct = i * g * (1 - fg ** (t + 1)) / (1 - fg)
         for bb in range(B):
             np.testing.assert_allclose(hs0[t, bb], o * np.tanh(ct), atol=1e-14)
+
+
+# ------------------------------------------------ non-residual alternative
+@pytest.mark.parametrize("G", [4, 1])
+def test_non_residual_terms_are_the_pruned_svd(G):
+    """Sec. III's alternative to the residual scheme: the terms are the
+    singular triplets of the original gate matrix (LAPACK SVD, sign rule
+    applied), each v pruned on its own."""
+    D, H = 10, 4
+    W, _, _ = rand_lstm(D, H, 501)
+    C, Rg = D + H, 4 * H // G
+    nz = 5
+    f = oracle.prepare(W, H, min(Rg, C), nz, groups=G, residual=False)
+    for g in range(G):
+        Ug, S, Vt = np.linalg.svd(W[g * Rg:(g + 1) * Rg])
+        np.testing.assert_allclose(f.sigma[g], S[:min(Rg, C)], rtol=1e-12)
+        for n in range(min(Rg, C)):
+            u, v = fix_sign(Ug[:, n], Vt[n])
+            np.testing.assert_allclose(f.U[g, n], u, atol=1e-10)
+            np.testing.assert_allclose(f.v_full[g, n], v, atol=1e-10)
+            assert np.array_equal(f.mask[g, n], oracle.magnitude_mask(v, nz))
+
+
+def test_residual_and_non_residual_coincide_without_pruning():
+    W, _, _ = rand_lstm(9, 3, 502)
+    a = oracle.prepare(W, 3, 12, 12, residual=True)
+    b = oracle.prepare(W, 3, 12, 12, residual=False)
+    np.testing.assert_allclose(a.sigma, b.sigma, rtol=1e-10, atol=1e-14)
+    assert np.array_equal(a.mask, b.mask)
+
+
+def test_residual_scheme_has_lower_weight_error_than_non_residual():
+    """The point of the residual scheme (Sec. III): with pruning, correcting
+    the pruning error in later terms gives a smaller weight error at the same
+    budget."""
+    w = synth.named("tiny")
+    a = oracle.prepare(w.W, 32, 32, 24, residual=True)
+    b = oracle.prepare(w.W, 32, 32, 24, residual=False)
+    W = w.W.astype(np.float64)
+    for K in (8, 16, 32):
+        ea = sum(np.linalg.norm(W[g * 32:(g + 1) * 32] - oracle.reconstruct(a, g, K)) ** 2 for g in range(4))
+        eb = sum(np.linalg.norm(W[g * 32:(g + 1) * 32] - oracle.reconstruct(b, g, K)) ** 2 for g in range(4))
+        assert ea < eb, (K, ea, eb)
