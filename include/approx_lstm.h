@@ -177,6 +177,39 @@ approx_lstm_status approx_lstm_run_deadline(approx_lstm_model* m, const float* x
                                             float* h_out, int32_t* k_achieved, float* step_us, void* hip_stream);
 
 /*
+ * approx_lstm_run_anytime -- progressive LSTM whose budget K_t is chosen
+ * online, on the device, at every timestep: the computation of each step is
+ * cut to what its share of the time budget allows (Sec. VI-B: predictions
+ * whose computation is cut short when the available time is used up; Sec. I:
+ * the best estimate for the time available).  One launch runs the sequence
+ * with room for every term of the model; at the end of timestep t workgroup
+ * 0 reads the device's wall clock and picks, among the candidate budgets
+ * K = 0, 1, 2, 4, ..., rank, the largest whose predicted step time still
+ * lets timestep t+1 end by (t+2) * deadline_us_per_step after the recurrence
+ * began (time saved by earlier steps is spent later, time lost is recovered
+ * by cutting later steps); the choice reaches every workgroup with the h
+ * exchange, so all compute with the same K_{t+1}.  K_0 is the largest
+ * candidate predicted to fit one deadline.
+ *
+ *   x, T, B, h0, c0  as for approx_lstm_run (T >= 1)
+ *   h_out            device [T][B][H]
+ *   k_achieved       host [T]: the K each timestep was computed with
+ *   step_us          host [T] or NULL: measured microseconds of every timestep
+ *
+ * fp32 models only (UNSUPPORTED for factor_dtype 1).  The predicted step
+ * times come from a calibration inside the same launch configuration (each
+ * candidate forced at every timestep), run on first use for a (T, B, launch
+ * width) and cached in the model.  Synchronises hip_stream.  Returns
+ * APPROX_LSTM_ERR_DEADLINE_INFEASIBLE if K = 0 is predicted to miss the
+ * deadline; otherwise the run completes (a step whose time ran out computes
+ * K = 0, and step_us tells whether the deadline was met).  The result equals
+ * a replay of the sequence with the reported k_achieved.
+ */
+approx_lstm_status approx_lstm_run_anytime(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                           const float* h0, const float* c0, double deadline_us_per_step,
+                                           float* h_out, int32_t* k_achieved, float* step_us, void* hip_stream);
+
+/*
  * approx_lstm_run_stack -- stacked LSTM layers, each progressive: layer l
  * (l >= 1) takes as its input sequence the h_t of layer l-1 at the same level.
  *

@@ -62,6 +62,7 @@ _sigs = {
     "approx_lstm_reserve": [_vp, _i32, _i32, _i32],
     "approx_lstm_run_stack": [_vp, _i32, _vp, _i32, _i32, _vp, _i32, _vp, _vp],
     "approx_lstm_run_deadline": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
+    "approx_lstm_run_anytime": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
     "approx_lstm_check": [_vp, _vp],
     "approx_lstm_set_launch": [_vp, _i32, _i32],
     "approx_lstm_model_info": [_vp, ctypes.POINTER(Info)],
@@ -176,6 +177,20 @@ def approx_lstm_run_deadline(model, x, deadline_us, h_out, h0=None, c0=None, str
     _check(st)
     return k, us
 
+
+
+def approx_lstm_run_anytime(model, x, deadline_us, h_out, h0=None, c0=None, stream=None):
+    """Budget chosen per timestep on the device.  x [T, B, D], h_out [T, B, H]
+    GPU float32.  Returns (k_achieved [T], step_us [T]) numpy arrays."""
+    T, B, D = x.shape
+    H = model.hidden_size
+    k = np.zeros(T, np.int32)
+    us = np.zeros(T, np.float32)
+    st = lib.approx_lstm_run_anytime(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)), _dev(c0, "c0", (B, H)),
+                                     float(deadline_us), _dev(h_out, "h_out", (T, B, H)), k.ctypes.data,
+                                     us.ctypes.data, ctypes.c_void_p(_stream(stream)))
+    _check(st)
+    return k, us
 
 def approx_lstm_run_stack(models, x, levels, h_out, stream=None):
     """models: list of Model; x [T, B, D0]; levels: [n_levels][n_layers] ints;

@@ -124,12 +124,18 @@ struct approx_lstm_model {
   // the (T, B, launch_blocks) it was measured at
   std::vector<std::pair<int, double>> calib;
   int calib_T = -1, calib_B = -1, calib_blocks = -1;
+  // online (anytime) calibration: microseconds per timestep against K inside
+  // the online launch (sized for the full rank), cached per (T, B, width)
+  std::vector<std::pair<int, double>> ocalib;
+  int ocalib_T = -1, ocalib_B = -1, ocalib_blocks = -1;
+  int* d_kt = nullptr;               // [kt_cap] budgets chosen by an online run
+  size_t kt_cap = 0;
   int launch_blocks = 0;             // 0 = automatic
   int cooperative = 0;               // 1: cooperative launch API
 
   ~approx_lstm_model() {
     if (!has_dev && !d_px && !d_zx && !d_hx && !d_hbx && !d_hflag && !d_err && !d_stamps && !d_stack && !d_bz &&
-        !d_bh && !d_bc)
+        !d_bh && !d_bc && !d_kt)
       return;
     DeviceScope ds(device);
     dfree(d_Vx);
@@ -151,6 +157,7 @@ struct approx_lstm_model {
     dfree(d_hflag);
     dfree(d_err);
     dfree(d_stamps);
+    dfree(d_kt);
     dfree(d_stack);
   }
 };
@@ -302,6 +309,104 @@ int auto_blocks(const approx_lstm_model* m, int GK, int LB, int LB_seq) {
     want = std::max(want, (m->H + rows_max - 1) / rows_max);
   }
   return std::max(1, std::min(cap, want));
+}
+
+// Budget options of an online run (see RunArgs::online).
+struct OnlineCfg {
+  int n = 0;
+  int k[alstm::kMaxOptions];
+  unsigned ticks[alstm::kMaxOptions];
+  unsigned long long budget = 0;
+};
+
+// The fp32 progressive run (argument checks done by the caller): fixed
+// levels, or with `on` one online level sized for the whole rank.
+approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t T, int32_t B, const float* h0,
+                                   const float* c0, const int32_t* levels, int32_t n_levels, int kmax, float* h_out,
+                                   float* c_out, hipStream_t stream, const OnlineCfg* on) {
+  alstm::RunArgs a{};
+  a.D = m->D; a.H = m->H; a.G = m->G; a.N = m->N; a.NZ = m->NZ; a.T = T; a.B = B; a.L = n_levels;
+  a.GK = m->G * kmax;
+  for (int l = 0; l < n_levels; ++l) a.levels[l] = levels[l];
+  if (on) {
+    // one level sized for the full rank; the kernel picks K_t per timestep
+    a.online = 1;
+    a.n_opts = on->n;
+    for (int i = 0; i < on->n; ++i) {
+      a.opt_k[i] = on->k[i];
+      a.opt_ticks[i] = on->ticks[i];
+    }
+    a.budget = on->budget;
+  }
+  a.hcap = a.GK > 0 ? m->hpre[a.GK - 1] : 0;
+  a.lanes_a = alstm::lanes_for_terms(m->NZ, m->D, m->H);
+  for (int l = 0; l < n_levels; ++l) a.lanes_b[l] = alstm::lanes_for_level(levels[l]);
+  const int maxP = std::max(1, m->num_cu);
+  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK, n_levels * B, B);
+  size_t lds = alstm::plan_progressive(a, P);
+  if (m->launch_blocks == 0)   // automatic: widen until the per-workgroup slices fit in LDS
+    while (lds > alstm::kLdsCap && P < maxP) {
+      P = std::min(maxP, 2 * P);
+      lds = alstm::plan_progressive(a, P);
+    }
+  const size_t LB = (size_t)n_levels * B;
+  if (lds > alstm::kLdsCap)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "LDS need %zu bytes exceeds 160 KiB (H=%d, levels*B=%zu, G*K=%d)",
+                lds, m->H, LB, a.GK);
+
+  const size_t kword = on ? 1 : 0;   // K_t of an online run rides with h
+  approx_lstm_status st =
+      ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * P * a.owned_max),
+                       LB * m->H + kword, stream);
+  if (st != APPROX_LSTM_OK) return st;
+  a.bulk_h = alstm::use_bulk_h(n_levels, B, m->H);
+  a.hb_stride = (int)round_up(LB * m->H + kword, 4);
+  if (a.bulk_h) {
+    st = ensure_bulk(m, 2 * (size_t)a.hb_stride, stream);
+    if (st != APPROX_LSTM_OK) return st;
+  }
+  m->seq = (m->seq + 1) & 0xFFFFu;
+  if (m->seq == 0) {
+    // tag space wrapped: clear the exchange words so no stale tag can match
+    HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
+    HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+    if (m->d_hflag)
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
+              "clear(hflag)");
+    m->seq = 1;
+  }
+  a.tag_base = m->seq << 16;
+  a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
+  a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
+  a.sigma = m->d_sigma; a.Ut = m->d_Ut; a.vidx = m->d_vidx; a.vval = m->d_vval; a.nx = m->d_nx;
+  a.bias = m->d_bias; a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx; a.err = m->d_err;
+  a.hbx = a.bulk_h ? m->d_hbx : nullptr;
+  a.hflag = a.bulk_h ? m->d_hflag : nullptr;
+  a.stamps = nullptr;
+  if (m->timing) {
+    const size_t words = 4 + 4 * (size_t)T;
+    if (words > m->stamps_cap) {
+      HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+      dfree(m->d_stamps);
+      m->stamps_cap = 0;
+      HIP_TRY(hipMalloc(&m->d_stamps, words * 8), "hipMalloc(stamps)");
+      m->stamps_cap = words;
+    }
+    a.stamps = m->d_stamps;
+    m->last_T = T;
+  }
+  if (on) {
+    if ((size_t)T > m->kt_cap) {
+      HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+      dfree(m->d_kt);
+      m->kt_cap = 0;
+      HIP_TRY(hipMalloc(&m->d_kt, (size_t)T * sizeof(int)), "hipMalloc(kt)");
+      m->kt_cap = T;
+    }
+    a.kt = m->d_kt;
+  }
+  HIP_TRY(alstm::launch_progressive(a, P, m->cooperative, stream), "launch progressive_lstm_kernel");
+  return APPROX_LSTM_OK;
 }
 
 }  // namespace
@@ -554,68 +659,7 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   hipStream_t stream = (hipStream_t)hip_stream;
   if (m->dtype == 1) return run_batched(m, x, T, B, h0, c0, levels, n_levels, h_out, c_out, stream);
 
-  alstm::RunArgs a{};
-  a.D = m->D; a.H = m->H; a.G = m->G; a.N = m->N; a.NZ = m->NZ; a.T = T; a.B = B; a.L = n_levels;
-  a.GK = m->G * kmax;
-  for (int l = 0; l < n_levels; ++l) a.levels[l] = levels[l];
-  a.hcap = a.GK > 0 ? m->hpre[a.GK - 1] : 0;
-  a.lanes_a = alstm::lanes_for_terms(m->NZ, m->D, m->H);
-  for (int l = 0; l < n_levels; ++l) a.lanes_b[l] = alstm::lanes_for_level(levels[l]);
-  const int maxP = std::max(1, m->num_cu);
-  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK, n_levels * B, B);
-  size_t lds = alstm::plan_progressive(a, P);
-  if (m->launch_blocks == 0)   // automatic: widen until the per-workgroup slices fit in LDS
-    while (lds > alstm::kLdsCap && P < maxP) {
-      P = std::min(maxP, 2 * P);
-      lds = alstm::plan_progressive(a, P);
-    }
-  const size_t LB = (size_t)n_levels * B;
-  if (lds > alstm::kLdsCap)
-    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "LDS need %zu bytes exceeds 160 KiB (H=%d, levels*B=%zu, G*K=%d)",
-                lds, m->H, LB, a.GK);
-
-  approx_lstm_status st =
-      ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * P * a.owned_max),
-                       LB * m->H, stream);
-  if (st != APPROX_LSTM_OK) return st;
-  a.bulk_h = alstm::use_bulk_h(n_levels, B, m->H);
-  a.hb_stride = (int)round_up(LB * m->H, 4);
-  if (a.bulk_h) {
-    st = ensure_bulk(m, 2 * (size_t)a.hb_stride, stream);
-    if (st != APPROX_LSTM_OK) return st;
-  }
-  m->seq = (m->seq + 1) & 0xFFFFu;
-  if (m->seq == 0) {
-    // tag space wrapped: clear the exchange words so no stale tag can match
-    HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
-    HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
-    if (m->d_hflag)
-      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
-              "clear(hflag)");
-    m->seq = 1;
-  }
-  a.tag_base = m->seq << 16;
-  a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
-  a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
-  a.sigma = m->d_sigma; a.Ut = m->d_Ut; a.vidx = m->d_vidx; a.vval = m->d_vval; a.nx = m->d_nx;
-  a.bias = m->d_bias; a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx; a.err = m->d_err;
-  a.hbx = a.bulk_h ? m->d_hbx : nullptr;
-  a.hflag = a.bulk_h ? m->d_hflag : nullptr;
-  a.stamps = nullptr;
-  if (m->timing) {
-    const size_t words = 4 + 4 * (size_t)T;
-    if (words > m->stamps_cap) {
-      HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
-      dfree(m->d_stamps);
-      m->stamps_cap = 0;
-      HIP_TRY(hipMalloc(&m->d_stamps, words * 8), "hipMalloc(stamps)");
-      m->stamps_cap = words;
-    }
-    a.stamps = m->d_stamps;
-    m->last_T = T;
-  }
-  HIP_TRY(alstm::launch_progressive(a, P, m->cooperative, stream), "launch progressive_lstm_kernel");
-  return APPROX_LSTM_OK;
+  return run_progressive(m, x, T, B, h0, c0, levels, n_levels, kmax, h_out, c_out, stream, nullptr);
 }
 
 approx_lstm_status approx_lstm_run_stack(approx_lstm_model* const* layers, int32_t n_layers, const float* x, int32_t T,
@@ -810,6 +854,85 @@ approx_lstm_status approx_lstm_run_deadline(approx_lstm_model* m, const float* x
     k_achieved[t] = lo;
     if (step_us) step_us[t] = (float)steps[t];
   }
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_run_anytime(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                           const float* h0, const float* c0, double deadline_us_per_step,
+                                           float* h_out, int32_t* k_achieved, float* step_us, void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (!m->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "model has no device store (HOST_ONLY)");
+  if (T < 1 || B < 1 || !x || !h_out || !k_achieved) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
+  if (T > 65534) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T = %d exceeds 65534", T);
+  if (!(deadline_us_per_step > 0.0)) return fail(APPROX_LSTM_ERR_INVALID_ARG, "deadline must be > 0");
+  if (m->dtype != 0) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "anytime mode needs an fp32 model");
+  DeviceScope ds(m->device);
+  if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  hipStream_t stream = (hipStream_t)hip_stream;
+  int khz = 0;
+  HIP_TRY(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, m->device), "wall clock rate");
+  if (khz <= 0) return fail(APPROX_LSTM_ERR_DEVICE, "device reports no wall clock rate");
+  const int32_t full = m->N;
+  const int saved_timing = m->timing;
+  m->timing = 1;
+  auto run_online = [&](const OnlineCfg& cfg, double* mean, std::vector<double>* steps) -> approx_lstm_status {
+    approx_lstm_status s = run_progressive(m, x, T, B, h0, c0, &full, 1, full, h_out, nullptr, stream, &cfg);
+    if (s != APPROX_LSTM_OK) return s;
+    std::vector<double> tmp;
+    s = per_step_us(m, hip_stream, T, steps ? *steps : tmp, mean);
+    if (s != APPROX_LSTM_OK) return s;
+    return approx_lstm_check(m, hip_stream);
+  };
+  approx_lstm_status st = APPROX_LSTM_OK;
+  // calibration inside the online launch: each candidate K forced at every
+  // timestep (cached for this T, B and launch width)
+  if (m->ocalib_T != T || m->ocalib_B != B || m->ocalib_blocks != m->launch_blocks || m->ocalib.empty()) {
+    m->ocalib.clear();
+    std::vector<int> ks{0};
+    for (int k = 1; k < m->N; k *= 2) ks.push_back(k);
+    ks.push_back(m->N);
+    while ((int)ks.size() > alstm::kMaxOptions) ks.erase(ks.begin() + 1);   // drop the smallest positive K
+    for (int k : ks) {
+      OnlineCfg cfg;
+      cfg.n = 1;
+      cfg.k[0] = k;
+      cfg.ticks[0] = 0;
+      cfg.budget = 1ull << 40;
+      double us = 0.0;
+      st = run_online(cfg, &us, nullptr);
+      if (st != APPROX_LSTM_OK) break;
+      m->ocalib.emplace_back(k, us);
+    }
+    if (st != APPROX_LSTM_OK) {
+      m->ocalib.clear();
+      m->timing = saved_timing;
+      return st;
+    }
+    m->ocalib_T = T;
+    m->ocalib_B = B;
+    m->ocalib_blocks = m->launch_blocks;
+  }
+  if (m->ocalib[0].second > deadline_us_per_step) {
+    m->timing = saved_timing;
+    return fail(APPROX_LSTM_ERR_DEADLINE_INFEASIBLE, "K = 0 takes %.3f us per timestep, above %.3f",
+                m->ocalib[0].second, deadline_us_per_step);
+  }
+  OnlineCfg cfg;
+  cfg.n = (int)m->ocalib.size();
+  for (int i = 0; i < cfg.n; ++i) {
+    cfg.k[i] = m->ocalib[i].first;
+    cfg.ticks[i] = (unsigned)std::ceil(m->ocalib[i].second * khz / 1000.0);
+  }
+  cfg.budget = (unsigned long long)std::floor(deadline_us_per_step * khz / 1000.0);
+  std::vector<double> steps;
+  double mean = 0.0;
+  st = run_online(cfg, &mean, &steps);
+  m->timing = saved_timing;
+  if (st != APPROX_LSTM_OK) return st;
+  HIP_TRY(hipMemcpy(k_achieved, m->d_kt, (size_t)T * sizeof(int32_t), hipMemcpyDeviceToHost), "read budgets");
+  if (step_us)
+    for (int t = 0; t < T; ++t) step_us[t] = (float)steps[t];
   return APPROX_LSTM_OK;
 }
 

@@ -104,14 +104,15 @@ struct Layout {
 
 __host__ __device__ inline size_t align16(size_t b) { return (b + 15) & ~(size_t)15; }
 
-__host__ __device__ inline Layout layout_of(const RunArgs& a) {
+__host__ __device__ inline Layout layout_of(const RunArgs& a, int online) {
   Layout l;
   const size_t LB = (size_t)a.L * a.B;
   const size_t kmax = a.G > 0 ? (size_t)a.GK / a.G : 0;
   size_t o = 0;
   // z of one (level, seq), [g][Kmax]; a single workgroup keeps every pair's
   l.zs = o;     o = align16(o + 4 * (a.P == 1 ? LB : 1) * (a.GK > 1 ? (size_t)a.GK : 1));
-  l.hs = o;     o = align16(o + 4 * LB * a.H);                        // h_{t-1} per (level, seq)
+  // h_{t-1} per (level, seq); an online run receives K_t in one more slot
+  l.hs = o;     o = align16(o + 4 * (LB * a.H + (online ? 1 : 0)));
   l.ys = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // y of the owned rows
   l.bs = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // bias of the owned rows
   l.cs = o;     o = align16(o + 4 * LB * a.rows_per);                 // c of the owned rows
@@ -136,10 +137,12 @@ __host__ __device__ inline Layout layout_of(const RunArgs& a) {
 // LDS.  UPT > 0: each phase-B thread keeps UPT entries of each of OPT output
 // rows in registers (requires one budget K for all levels, S*UPT >= K and
 // 4*rows_per*S <= 512*OPT); 0: U rows in LDS (ustride > 0) or from global.
-template <int HPL, int OPT, int UPT>
+// ONLINE: one level whose budget is chosen per timestep (RunArgs::online);
+// the fixed-budget kernels carry none of its code.
+template <int HPL, int OPT, int UPT, bool ONLINE>
 __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
-  const Layout L = layout_of(a);
+  const Layout L = layout_of(a, ONLINE ? 1 : 0);
   const int P = gridDim.x, j = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int D = a.D, H = a.H, G = a.G, N = a.N, NZ = a.NZ, T = a.T, B = a.B;
@@ -277,6 +280,18 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     a.stamps[0] = wall_clock64();
     a.stamps[1] = clock64();
   }
+  // online run: the same thread of workgroup 0 keeps the clock and chooses;
+  // K_0 is the choice for one budget, the same in every workgroup
+  const bool chooser = ONLINE && j == 0 && (int)threadIdx.x == kThreads - 64;
+  unsigned long long t_begin = 0ull;
+  int kcur = 0;
+  if constexpr (ONLINE) {
+    kcur = online_pick(a, (long long)a.budget);
+    if (chooser) {
+      t_begin = wall_clock64();
+      a.kt[0] = kcur;
+    }
+  }
   for (int t = 0; t < T; ++t) {
     const unsigned tag = a.tag_base | (unsigned)(t + 1);
     const float* pxc = pxb + (a.px_all ? t : (t & 1)) * B * OM;
@@ -285,7 +300,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     // ---- phase A: z = sigma * (P_x + prune(v)_h . h_{t-1}) for the owned terms ----
     for (int lb = 0; lb < LB; ++lb) {
       const int l = lb / B, b = lb % B;
-      const int GKl = G * a.levels[l];
+      const int GKl = G * (ONLINE ? kcur : a.levels[l]);
       const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
       const float* h = hs + lb * H;
       if constexpr (HPL > 0) {
@@ -328,7 +343,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     if (stamp) a.stamps[3 + 4 * t] = clock64();
     if (publisher && !local) {
       for (int lb = 0; lb < LB; ++lb) {
-        const int GKl = G * a.levels[lb / B];
+        const int GKl = G * (ONLINE ? kcur : a.levels[lb / B]);
         const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
         for (int i = lane; i < nl; i += 64)
           publish(a.zx + (size_t)lb * P * OM + j * OM + i, zown[lb * OM + i], tag);
@@ -339,7 +354,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     if (rc > 0) {
       for (int lb = 0; lb < LB; ++lb) {
         const int l = lb / B;
-        const int Kl = a.levels[l];
+        const int Kl = ONLINE ? kcur : a.levels[l];
         if (!local && !publisher) {
           // P_x of the next timestep travels while the z words are awaited
           if (!a.px_all && lb == 0 && t + 1 < T) {
@@ -421,6 +436,16 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     // without terms (every level K = 0) no workgroup reads another's h
     const bool exch = !local && GK > 0;
     float* hbt = a.bulk_h ? a.hbx + (size_t)(t & 1) * a.hb_stride : nullptr;
+    if (ONLINE && chooser && t + 1 < T) {
+      // K_{t+1}: timestep t+1 must end by (t+2) * budget after the start
+      const long long used = (long long)(wall_clock64() - t_begin);
+      const int knext = online_pick(a, (long long)(t + 2) * (long long)a.budget - used);
+      a.kt[t + 1] = knext;
+      const float kbits = __int_as_float(knext);
+      if (local) hs[LB * H] = kbits;
+      else if (a.bulk_h) store_coherent(hbt + (size_t)LB * H, kbits);
+      else publish(a.hx + (size_t)LB * H, kbits, tag);
+    }
     if (publisher) {
       for (int lb = 0; lb < LB; ++lb) {
         const int l = lb / B, b = lb % B;
@@ -440,7 +465,8 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
       }
     }
 
-    // ---- phase C: gather h_t ----
+    // ---- phase C: gather h_t (and K_{t+1} of an online run) ----
+    const int online_word = (ONLINE && t + 1 < T) ? 1 : 0;
     if (exch) {
       if (a.bulk_h) {
         // h_t is double-buffered by step parity: a workgroup can publish
@@ -448,12 +474,13 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
         // has finished reading h_t
         if (!publisher) await_flags(a.hflag, P, tag, a.err, threadIdx.x, gthr);
         lds_barrier();
-        if (!publisher) read_coherent(hs, hbt, LB * H, threadIdx.x, gthr);
+        if (!publisher) read_coherent(hs, hbt, LB * H + online_word, threadIdx.x, gthr);
       } else if (!publisher) {
-        gather_tagged<2>(hs, nullptr, a.hx, LB * H, tag, a.err, threadIdx.x, gthr);
+        gather_tagged<2>(hs, nullptr, a.hx, LB * H + online_word, tag, a.err, threadIdx.x, gthr);
       }
     }
     lds_barrier();
+    if (ONLINE && t + 1 < T) kcur = __float_as_int(hs[LB * H]);
   }
   if (stamp) {
     a.stamps[2 + 4 * T] = clock64();
@@ -667,31 +694,35 @@ size_t plan_progressive(RunArgs& a, int P) {
     // 64 U entries per thread only next to at most 8 h-part entries per
     // lane: beyond that the register file (256 per lane) spills
     if (a.upt == 64 && a.hpl > 8) { a.opt = 0; a.upt = 0; }
+    // online runs are built for one output row per thread and up to 32 U
+    // entries in registers only, 32 of them next to at most 12 h-part
+    // entries per lane (more spills)
+    if (a.online && (a.opt != 1 || a.upt > 32 || (a.upt == 32 && a.hpl > 12))) { a.opt = 0; a.upt = 0; }
   }
   a.P = P;
   a.vh_lds = 0;
   a.ustride = 0;
   a.px_all = 0;
-  size_t need = layout_of(a).total;
+  size_t need = layout_of(a, a.online).total;
   if (need > kLdsCap) return need;
   if (a.hpl == 0) {
     a.vh_lds = 1;
-    if (layout_of(a).total > kLdsCap) return layout_of(a).total;   // h-part entries must fit
+    if (layout_of(a, a.online).total > kLdsCap) return layout_of(a, a.online).total;   // h-part entries must fit
   }
   if (a.upt == 0 && Kmax > 0) {
     // stride = smax * odd: the lanes of consecutive rows hit distinct banks
     a.ustride = smax * ((((Kmax + smax - 1) / smax)) | 1);
-    if (layout_of(a).total > kLdsCap) a.ustride = 0;
+    if (layout_of(a, a.online).total > kLdsCap) a.ustride = 0;
   }
   a.px_all = 1;
-  if (layout_of(a).total > kLdsCap) a.px_all = 0;
-  return layout_of(a).total;
+  if (layout_of(a, a.online).total > kLdsCap) a.px_all = 0;
+  return layout_of(a, a.online).total;
 }
 
-template <int HPL, int OPT, int UPT>
+template <int HPL, int OPT, int UPT, bool ONLINE = false>
 hipError_t launch_one(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
   static bool attr_set = false;
-  const void* fn = (const void*)progressive_lstm_kernel<HPL, OPT, UPT>;
+  const void* fn = (const void*)progressive_lstm_kernel<HPL, OPT, UPT, ONLINE>;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsCap);
     if (e != hipSuccess) return e;
@@ -702,12 +733,19 @@ hipError_t launch_one(const RunArgs& a, int blocks, int cooperative, size_t lds,
     void* args[] = {&copy};
     return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(kThreads), args, (unsigned)lds, stream);
   }
-  progressive_lstm_kernel<HPL, OPT, UPT><<<dim3(blocks), dim3(kThreads), lds, stream>>>(a);
+  progressive_lstm_kernel<HPL, OPT, UPT, ONLINE><<<dim3(blocks), dim3(kThreads), lds, stream>>>(a);
   return hipGetLastError();
 }
 
 template <int HPL>
 hipError_t launch_u(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
+  if (a.online) {   // the planner keeps online runs to these shapes
+    if (a.opt == 1 && a.upt == 8) return launch_one<HPL, 1, 8, true>(a, blocks, cooperative, lds, stream);
+    if (a.opt == 1 && a.upt == 16) return launch_one<HPL, 1, 16, true>(a, blocks, cooperative, lds, stream);
+    if constexpr (HPL <= 12)
+      if (a.opt == 1 && a.upt == 32) return launch_one<HPL, 1, 32, true>(a, blocks, cooperative, lds, stream);
+    return launch_one<HPL, 1, 0, true>(a, blocks, cooperative, lds, stream);
+  }
   if (a.opt == 1 && a.upt == 8) return launch_one<HPL, 1, 8>(a, blocks, cooperative, lds, stream);
   if (a.opt == 1 && a.upt == 16) return launch_one<HPL, 1, 16>(a, blocks, cooperative, lds, stream);
   if (a.opt == 1 && a.upt == 32) return launch_one<HPL, 1, 32>(a, blocks, cooperative, lds, stream);
@@ -746,7 +784,7 @@ hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hip
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const size_t lds = layout_of(a).total;
+  const size_t lds = layout_of(a, a.online).total;
   switch (a.hpl) {
     case 4: return launch_u<4>(a, blocks, cooperative, lds, stream);
     case 8: return launch_u<8>(a, blocks, cooperative, lds, stream);

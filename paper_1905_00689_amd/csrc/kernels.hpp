@@ -7,6 +7,7 @@
 namespace alstm {
 
 constexpr int kMaxLevels = 16;
+constexpr int kMaxOptions = 24;        // candidate budgets of an online (anytime) run
 constexpr int kThreads = 512;          // 8 wave64 per workgroup
 constexpr int kMaxXChunk = 16;         // (t, b) pairs accumulated per pass of the input projection
 constexpr size_t kLdsCap = 160 * 1024; // LDS per CU on gfx950
@@ -69,7 +70,28 @@ struct RunArgs {
   unsigned tag_base;
   int levels[kMaxLevels];
   int lanes_b[kMaxLevels];  // lanes per output row in phase B, per level (a function of K only)
+  // online (anytime) run: one level of up to levels[0] terms whose budget K_t
+  // is chosen per timestep on the device.  Workgroup 0 reads the wall clock
+  // (100 MHz) at the end of timestep t's gate update and takes the largest
+  // option whose predicted timestep still ends by (t+2) * budget ticks after
+  // the recurrence began; the choice travels to every workgroup as one more
+  // word of the h exchange (slot L*B*H), so all agree on K_{t+1}.
+  int online;                       // 0: fixed levels
+  int n_opts;                       // options, K ascending
+  int opt_k[kMaxOptions];           // candidate budgets
+  unsigned opt_ticks[kMaxOptions];  // predicted wall ticks of one timestep at that budget
+  unsigned long long budget;        // wall ticks per timestep
+  int* kt;                          // [T] chosen budgets (written by workgroup 0)
 };
+
+// Budget of an online run for `avail` wall ticks: the largest option that
+// fits, else the smallest.
+__host__ __device__ inline int online_pick(const RunArgs& a, long long avail) {
+  int k = a.opt_k[0];
+  for (int i = 0; i < a.n_opts; ++i)
+    if ((long long)a.opt_ticks[i] <= avail) k = a.opt_k[i] > k ? a.opt_k[i] : k;
+  return k;
+}
 
 // Reduction shapes.  They depend only on the model (phase A) and on each
 // level's own budget (phase B), never on the launch width or on the other
