@@ -56,6 +56,9 @@ def main():
                     help="only time a plain 256 MiB device copy (reference for HBM counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--batched-sweep", default="32,128,512", help="K values timed in the batched workload")
+    ap.add_argument("--time-prepare", default="",
+                    help="NAME:RANK:PRUNE -- only time the device factorisation of a named workload "
+                         "(e.g. deadline:2048:0.9) and print one JSON line")
     ap.add_argument("--workload", default="driving", choices=["driving", "batched"],
                     help="driving: batch 1, fp32 (default line); batched: 256 sequences, bf16 MFMA path")
     args = ap.parse_args()
@@ -73,6 +76,9 @@ def main():
     from paper_1905_00689_amd import binding as B
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.time_prepare:
+        time_prepare(args.time_prepare, torch, synth, B)
+        return
     if args.workload == "batched":
         bench_batched(args, torch)
         return
@@ -332,6 +338,22 @@ def anytime_comparison(torch, B, stream):
     return out
 
 
+def time_prepare(spec, torch, synth, B):
+    """Wall time of approx_lstm_prepare with the factorisation on the device
+    (APPROX_LSTM_FLAG_DEVICE_FACTORISE) for a named synthetic workload."""
+    name, rank, prune = spec.split(":")
+    w = synth.named(name)
+    torch.cuda.init()
+    t0 = time.time()
+    m = B.approx_lstm_prepare(w.W[:, :w.D], w.W[:, w.D:], w.b, w.D, w.H, int(rank), prune_ratio=float(prune),
+                              flags=B.FLAG_DEVICE_FACTORISE)
+    sec = time.time() - t0
+    inf = m.info
+    print(json.dumps({"prepare": f"device factorisation, {name} D={w.D} H={w.H} rank {rank} prune {prune}",
+                      "seconds": round(sec, 3), "nz": inf["nz"], "eff_rank": inf["eff_rank"],
+                      "unconverged_steps": inf["unconverged_steps"]}), flush=True)
+
+
 def step_distribution(torch, step, stream, n):
     """Per-step times (ms) of n further steps, each between its own pair of
     events on the launch stream: median, p99 and max (the headline value
@@ -479,23 +501,31 @@ def oracle_threads():
 
 
 TRAFFIC_PROFILES = {
-    "driving": ("driving_K512_p75_hbm_counters.md", "kernels.hip"),
-    "batched": ("batched_K512_p75_hbm_counters.md", "batched.hip"),
+    "driving": ("driving_K512_p75_hbm_counters.md", ("kernels.hip", "kernels.hpp", "device_common.hpp")),
+    "batched": ("batched_K512_p75_hbm_counters.md", ("batched.hip", "kernels.hpp", "device_common.hpp")),
 }
+
+
+def kernel_sources_sha256(names):
+    """sha256 over the named kernel sources, concatenated in order."""
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    h = hashlib.sha256()
+    for n in names:
+        h.update(open(os.path.join(root, "paper_1905_00689_amd", "csrc", n), "rb").read())
+    return h.hexdigest()
 
 
 def measured_traffic(workload):
     """HBM bytes per step from the committed rocprofv3 counter summary of the
-    workload, if it was taken on the kernel source as it is now (else None)."""
-    import hashlib
+    workload, if it was taken on the kernel sources as they are now (else
+    None)."""
     root = os.path.dirname(os.path.abspath(__file__))
-    prof_name, src_name = TRAFFIC_PROFILES[workload]
+    prof_name, src_names = TRAFFIC_PROFILES[workload]
     prof = os.path.join(root, "profiles", prof_name)
-    src = os.path.join(root, "paper_1905_00689_amd", "csrc", src_name)
     try:
         fields = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if ": " in l and not l.startswith(" "))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-        if fields.get("kernel_source_sha256", "").strip() != sha:
+        if fields.get("kernel_sources_sha256", "").strip() != kernel_sources_sha256(src_names):
             return None
         return int(fields["traffic_bytes_per_step"])
     except (OSError, KeyError, ValueError):
