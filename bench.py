@@ -59,8 +59,9 @@ def main():
     ap.add_argument("--time-prepare", default="",
                     help="NAME:RANK:PRUNE -- only time the device factorisation of a named workload "
                          "(e.g. deadline:2048:0.9) and print one JSON line")
-    ap.add_argument("--workload", default="driving", choices=["driving", "batched"],
-                    help="driving: batch 1, fp32 (default line); batched: 256 sequences, bf16 MFMA path")
+    ap.add_argument("--workload", default="driving", choices=["driving", "batched", "deadline"],
+                    help="driving: batch 1, fp32 (default line); batched: 256 sequences, bf16 MFMA path; "
+                         "deadline: D=H=2048, T=64, 8 sequences, rank 2048, both deadline modes")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -81,6 +82,9 @@ def main():
         return
     if args.workload == "batched":
         bench_batched(args, torch)
+        return
+    if args.workload == "deadline":
+        bench_deadline(args, torch)
         return
     dev = torch.device("cuda")
     wl = synth.named("driving")
@@ -336,6 +340,91 @@ def anytime_comparison(torch, B, stream):
                                   [(128, 4160), (128, 130), (128, 32), (64, 4160, "non-residual"),
                                    (64, 130, "non-residual")], Kp, rows_p)
     return out
+
+
+def bench_deadline(args, torch):
+    """The deadline workload (D=2048, H=2048, T=64, 8 sequences, per-gate rank
+    2048, 90% pruning, fp32).  The factorisation runs on the device; then
+    fixed budgets are timed, and both deadline modes run at 5, 20 and 100 us
+    per timestep: one K for the sequence (approx_lstm_run_deadline) and K_t
+    chosen per timestep on the device (approx_lstm_run_anytime).  Each
+    reports the budgets achieved, the measured step times and the output's
+    error against the device's exact LSTM on the same input (see _qor)."""
+    from paper_1905_00689_amd import synth
+    from paper_1905_00689_amd import binding as B
+    dev = torch.device("cuda")
+    wl = synth.named("deadline")
+    D, H, T, Bn = wl.D, wl.H, wl.T, wl.B
+    rank = 2048
+    t0 = time.time()
+    m = B.approx_lstm_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H, rank, prune_ratio=0.9, groups=4,
+                              flags=B.FLAG_DEVICE_FACTORISE)
+    prep_s = time.time() - t0
+    x = torch.from_numpy(wl.x).to(dev)
+    stream = torch.cuda.current_stream()
+    me = B.approx_lstm_exact_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H)
+    href = torch.empty((T, Bn, H), device=dev)
+    B.approx_lstm_exact_run(me, x, href, stream=stream)
+    torch.cuda.synchronize()
+    B.approx_lstm_exact_check(me)
+    quality = _qor(synth.softmax_head(H).astype(np.float64), href.cpu().numpy().astype(np.float64))
+
+    def timed(fn, steps=10):
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps   # ms per run
+
+    h1 = torch.empty((1, T, Bn, H), device=dev)
+    fixed = {"K": [], "us_per_timestep": [], "rel_err": [], "kl": []}
+    for k in (0, 1, 16, 256, 1024, 2048):
+        ms = timed(lambda: B.approx_lstm_run(m, x, [k], h1, stream=stream))
+        B.approx_lstm_check(m)
+        e, kl = quality(h1[0].cpu().numpy())
+        fixed["K"].append(k)
+        fixed["us_per_timestep"].append(round(ms * 1e3 / T, 3))
+        fixed["rel_err"].append(_sig(e))
+        fixed["kl"].append(_sig(kl))
+    ms_exact = timed(lambda: B.approx_lstm_exact_run(me, x, href, stream=stream))
+
+    modes = {}
+    h = torch.empty((T, Bn, H), device=dev)
+    for name, fn in (("one_K", B.approx_lstm_run_deadline), ("anytime", B.approx_lstm_run_anytime)):
+        rows = []
+        for dl in (5.0, 20.0, 100.0):
+            try:
+                k, us = fn(m, x, dl, h, stream=stream)
+            except B.ApproxLstmError as err:
+                if err.status != B.ERR_DEADLINE_INFEASIBLE:
+                    raise
+                rows.append({"deadline_us": dl, "status": "infeasible", "detail": str(err).split(": ", 1)[-1]})
+                continue
+            e, kl = quality(h.cpu().numpy())
+            rows.append({"deadline_us": dl, "status": "ok", "k_mean": round(float(np.mean(k)), 1),
+                         "k_min": int(np.min(k)), "k_max": int(np.max(k)),
+                         "step_us_mean": round(float(np.mean(us)), 3), "step_us_max": round(float(np.max(us)), 3),
+                         "steps_within_deadline": round(float(np.mean(us <= dl)), 3),
+                         "rel_err": _sig(e), "kl": _sig(kl)})
+        modes[name] = rows
+    value = T * Bn / (fixed["us_per_timestep"][-1] * 1e-6 * T)
+    out = {
+        "metric": "deadline mode: achieved K, step time and error vs the exact LSTM at per-timestep deadlines",
+        "value": round(value, 1), "unit": "timesteps/s at K=2048", "n_gpus": 1, "higher_is_better": True,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "deadline: D=2048 H=2048 T=64 B=8, per-gate rank 2048, 90% pruning (NZ=410)",
+                   "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": m.info["nz"]},
+        "prepare_device_s": round(prep_s, 2), "fixed_budgets": fixed,
+        "exact_us_per_timestep": round(ms_exact * 1e3 / T, 3), "deadline_modes": modes,
+        "note": "errors against the device's exact LSTM; 'steps_within_deadline' is the share of timesteps "
+                "whose measured time met the deadline",
+    }
+    print(json.dumps(out), flush=True)
 
 
 def time_prepare(spec, torch, synth, B):

@@ -15,6 +15,8 @@
 // the dense products stopped after that many rows of every gate, the rows
 // not reached holding the bias alone.  Only the computed rows are projected
 // and multiplied.
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -27,6 +29,7 @@ constexpr int kExactRows = kThreads / kExactLanes;   // rows per pass (32)
 constexpr int kExactWpl = 32;     // W_h entries per lane held in registers (H <= 512)
 constexpr int kExactCols = 16;    // x columns per staging pass of the x projection
 constexpr int kExactXprojRegs = 32;   // weights per lane of the x projection held in registers (D <= 2048)
+constexpr int kExactSeq = 8;      // sequences sharing one read of a W_h row in the recurrence
 
 }  // namespace
 
@@ -163,33 +166,95 @@ __global__ void __launch_bounds__(kThreads) exact_lstm_kernel(ExactArgs a) {
   const bool local = P == 1;
   const bool publisher = wave == kWaves - 1;
   const int gthr = kThreads - 64;
+  // y of owned row ol for sequence b: the W_h sum plus the x part and bias
+  auto store_y = [&](int t, int b, int ol, float sum) {
+    const int q = ol / rc, rr = ol - q * rc;
+    const int o = q * H + r0 + rr;
+    const float px = a.px_lds ? pxs[(t * B + b) * 4 * RP + ol]
+                              : (rr < rlive ? a.px[(size_t)(t * B + b) * R4 + o] : a.bias[o]);
+    ys[b * 4 * RP + ol] = sum + px;
+  };
   for (int t = 0; t < T; ++t) {
     const unsigned tag = a.tag_base | (unsigned)(t + 1);
-    for (int b = 0; b < B; ++b) {
-      const float* h = hs + (size_t)b * H;
-      for (int ps = 0; ps < passes; ++ps) {
-        const int ol = ob + ps * kExactRows;
-        float acc = 0.0f;
-        if (ol < outs) {
-          if (wreg && ps == 0) {
+    if (wreg) {
+      // pass 0's entries are in registers; later passes read their rows
+      for (int b = 0; b < B; ++b) {
+        const float* h = hs + (size_t)b * H;
+        for (int ps = 0; ps < passes; ++ps) {
+          const int ol = ob + ps * kExactRows;
+          float acc = 0.0f;
+          if (ol < outs) {
+            if (ps == 0) {
 #pragma unroll
-            for (int i = 0; i < kExactWpl; ++i) acc += wr[i] * h[min(sl + kExactLanes * i, H - 1)];
-          } else {
-            const int q = ol / rc, rr = ol - q * rc;
-            const float* wrow = a.Wh + (size_t)(q * H + r0 + rr) * H;
-            if (rr < rlive) {
+              for (int i = 0; i < kExactWpl; ++i) acc += wr[i] * h[min(sl + kExactLanes * i, H - 1)];
+            } else {
+              const int q = ol / rc, rr = ol - q * rc;
+              const float* wrow = a.Wh + (size_t)(q * H + r0 + rr) * H;
+              if (rr < rlive) {
 #pragma unroll 4
-              for (int k = sl; k < H; k += kExactLanes) acc += wrow[k] * h[k];
+                for (int k = sl; k < H; k += kExactLanes) acc += wrow[k] * h[k];
+              }
             }
           }
+          acc = group_sum<kExactLanes>(acc);
+          if (sl == 0 && ol < outs) store_y(t, b, ol, acc);
         }
-        acc = group_sum<kExactLanes>(acc);
-        if (sl == 0 && ol < outs) {
-          const int q = ol / rc, rr = ol - q * rc;
-          const int o = q * H + r0 + rr;
-          const float px = a.px_lds ? pxs[(t * B + b) * 4 * RP + ol]
-                                    : (rr < rlive ? a.px[(size_t)(t * B + b) * R4 + o] : a.bias[o]);
-          ys[b * 4 * RP + ol] = acc + px;
+      }
+    } else {
+      // rows are read once per group of up to kExactSeq sequences, each entry
+      // applied to every sequence of the group (NB a compile-time group size,
+      // so the inner loop carries no predicates); every (row, sequence) sum
+      // keeps the per-sequence order
+      auto group = [&](auto nbc, int b0) {
+        constexpr int NB = decltype(nbc)::value;
+        for (int ps = 0; ps < passes; ++ps) {
+          const int ol = ob + ps * kExactRows;
+          float acc[NB];
+#pragma unroll
+          for (int j = 0; j < NB; ++j) acc[j] = 0.0f;
+          if (ol < outs) {
+            const int q = ol / rc, rr = ol - q * rc;
+            const float* wrow = a.Wh + (size_t)(q * H + r0 + rr) * H;
+            if (rr < rlive && NB == 1) {
+#pragma unroll 4
+              for (int k = sl; k < H; k += kExactLanes) acc[0] += wrow[k] * hs[(size_t)b0 * H + k];
+            } else if (rr < rlive) {
+              // 8 entries of the row in flight, then each applied to the group
+              for (int k0 = sl; k0 < H; k0 += 8 * kExactLanes) {
+                float wk[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                  const int k = k0 + i * kExactLanes;
+                  wk[i] = wrow[k < H ? k : sl];
+                }
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                  const int k = k0 + i * kExactLanes;
+                  if (k < H) {
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) acc[j] += wk[i] * hs[(size_t)(b0 + j) * H + k];
+                  }
+                }
+              }
+            }
+          }
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            const float sum = group_sum<kExactLanes>(acc[j]);
+            if (sl == 0 && ol < outs) store_y(t, b0 + j, ol, sum);
+          }
+        }
+      };
+      for (int b0 = 0; b0 < B; b0 += kExactSeq) {
+        switch (min(kExactSeq, B - b0)) {
+          case 1: group(std::integral_constant<int, 1>{}, b0); break;
+          case 2: group(std::integral_constant<int, 2>{}, b0); break;
+          case 3: group(std::integral_constant<int, 3>{}, b0); break;
+          case 4: group(std::integral_constant<int, 4>{}, b0); break;
+          case 5: group(std::integral_constant<int, 5>{}, b0); break;
+          case 6: group(std::integral_constant<int, 6>{}, b0); break;
+          case 7: group(std::integral_constant<int, 7>{}, b0); break;
+          default: group(std::integral_constant<int, 8>{}, b0); break;
         }
       }
     }

@@ -154,3 +154,30 @@ def test_row_tile_rejects_out_of_range_budgets():
     for rows in (-1, 33):
         with pytest.raises(B.ApproxLstmError):
             B.approx_lstm_exact_run_rows(m, x, rows, h)
+
+
+def test_exact_grouped_rows_ragged_batch():
+    """H=600 (rows read from memory, not registers) with 11 sequences: each
+    W_h row is applied to groups of 8 and 3 sequences.  Every launch width
+    gives the same bits and the oracle's values; the row-tile variant too."""
+    w = synth.make(40, 600, 4, 11, index=33, xkind="relu")
+    rng = np.random.default_rng(10)
+    h0 = rng.normal(size=(11, 600)).astype(np.float32)
+    c0 = rng.normal(size=(11, 600)).astype(np.float32)
+    m = exact_model(w)
+    for rows in (None, 250):
+        if rows is None:
+            he, ce = oracle.exact_lstm(w.W, w.b, w.x, h0, c0)
+        else:
+            he, ce = oracle.row_tile_lstm(w.W, w.b, w.x, rows, h0, c0)
+        ref = None
+        for P in (0, 7, 75):
+            say("exact grouped rows, rows", rows, "blocks", P)
+            B.approx_lstm_exact_set_launch(m, P)
+            h, c = run_exact(m, w.x, h0, c0, want_c=True, rows=rows)
+            assert rel_err(h, he) < TOL, (rows, P)
+            assert np.abs(c - ce).max() < TOL * max(1.0, np.abs(ce).max()), (rows, P)
+            if ref is None:
+                ref = h
+            else:
+                assert np.array_equal(h, ref), (rows, P)

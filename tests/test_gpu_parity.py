@@ -387,3 +387,4 @@ def test_paper_shape_matches_oracle(paper, nz):
         e = rel_err(h[1 + j], ho[j])
         say("  K", K, "rel err (oracle factors)", e)
         assert e < TOL, (K, e)
+
