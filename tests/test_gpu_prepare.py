@@ -133,8 +133,9 @@ def test_device_prepare_rejects_host_only():
 def test_deadline_workload_full_rank_on_device():
     """The deadline workload at its full size (D=2048, H=2048, 90% pruning,
     rank 2048 per gate), factorised on the device: one-step parity at steps
-    across the chain of one gate, then runs at K = 1 and 2048 against the
-    oracle on the exported terms (T=64, 8 sequences)."""
+    at the first and the last step of one gate's chain, then runs at K = 1
+    and 512 against the oracle on the exported terms (T=64, 8 sequences).
+    Sized to finish in about two minutes."""
     w = synth.named("deadline")
     say("device prepare deadline rank 2048 p=0.9")
     t0 = time.time()
@@ -148,7 +149,7 @@ def test_deadline_workload_full_rank_on_device():
     l64 = B.approx_lstm_get_factors_f64(m, g)
     say("  one-step parity, gate", g)
     res = check_steps(W[g * 2048:(g + 1) * 2048], l64["sigma"], l64["u"], l64["v"],
-                      lf["v_idx"].astype(np.int64), inf["nz"], [0, 1024, 2047],
+                      lf["v_idx"].astype(np.int64), inf["nz"], [0, 2047],
                       progress=lambda n: say("    step", n, "checked"))
     assert all(s == "exact" for _, s in res), res
     # one level per run: at H = 2048 with 8 sequences the recurrence's LDS
@@ -156,7 +157,7 @@ def test_deadline_workload_full_rank_on_device():
     f = exported_factors(m)
     x = torch.from_numpy(w.x).cuda()
     h = torch.full((1, w.T, w.B, w.H), float("nan"), device="cuda")
-    for K in (1, 2048):
+    for K in (1, 512):
         say("  run K", K, "vs oracle on exported terms")
         B.approx_lstm_run(m, x, [K], h)
         B.approx_lstm_check(m)
