@@ -139,9 +139,16 @@ __global__ void __launch_bounds__(kFT) symv_kernel(const double* __restrict__ G,
   if (i >= n) return;
   const double* a = G + g * sG + (size_t)i * n;
   const double* q = Q + g * sQ + (size_t)k * n;
-  double acc = 0.0;
-  for (int j = lane; j < n; j += 64) acc = fma(a[j], q[j], acc);
-  acc = wave_sum_f64(acc);
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  int j = lane;
+  for (; j + 192 < n; j += 256) {
+    a0 = fma(a[j], q[j], a0);
+    a1 = fma(a[j + 64], q[j + 64], a1);
+    a2 = fma(a[j + 128], q[j + 128], a2);
+    a3 = fma(a[j + 192], q[j + 192], a3);
+  }
+  for (; j < n; j += 64) a0 = fma(a[j], q[j], a0);
+  const double acc = wave_sum_f64((a0 + a1) + (a2 + a3));
   if (lane == 0) w[(size_t)g * n + i] = acc;
 }
 
@@ -157,9 +164,18 @@ __global__ void __launch_bounds__(kFT) dots_kernel(const double* __restrict__ Q,
   const double* wg = w + (size_t)g * n;
   for (int j = blockIdx.x * kFW + (threadIdx.x >> 6); j <= k; j += gridDim.x * kFW) {
     const double* q = Q + g * sQ + (size_t)j * n;
-    double acc = 0.0;
-    for (int i = lane; i < n; i += 64) acc = fma(q[i], wg[i], acc);
-    acc = wave_sum_f64(acc);
+    // four independent partial sums per lane (more loads in flight), added
+    // in a fixed order
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+    int i = lane;
+    for (; i + 192 < n; i += 256) {
+      a0 = fma(q[i], wg[i], a0);
+      a1 = fma(q[i + 64], wg[i + 64], a1);
+      a2 = fma(q[i + 128], wg[i + 128], a2);
+      a3 = fma(q[i + 192], wg[i + 192], a3);
+    }
+    for (; i < n; i += 64) a0 = fma(q[i], wg[i], a0);
+    const double acc = wave_sum_f64((a0 + a1) + (a2 + a3));
     if (lane == 0) c[g * sc + j] = acc;
   }
 }
@@ -183,10 +199,17 @@ __global__ void __launch_bounds__(kFT) combine_kernel(const double* __restrict__
   const int nv = cnts[g] + add_one;
   const double* Qg = Q + g * sQ;
   const double* cg = c + g * sc;
-  double acc = 0.0;
-  if (i < n)
-    for (int j = wave; j < nv; j += kFW) acc = fma(cg[j], Qg[(size_t)j * n + i], acc);
-  part[wave][lane] = acc;
+  // two independent partial sums per lane, added in a fixed order
+  double a0 = 0.0, a1 = 0.0;
+  if (i < n) {
+    int j = wave;
+    for (; j + kFW < nv; j += 2 * kFW) {
+      a0 = fma(cg[j], Qg[(size_t)j * n + i], a0);
+      a1 = fma(cg[j + kFW], Qg[(size_t)(j + kFW) * n + i], a1);
+    }
+    if (j < nv) a0 = fma(cg[j], Qg[(size_t)j * n + i], a0);
+  }
+  part[wave][lane] = a0 + a1;
   __syncthreads();
   if (wave == 0 && i < n) {
     double s = 0.0;
