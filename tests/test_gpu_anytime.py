@@ -118,3 +118,34 @@ def test_anytime_single_workgroup():
     m = prep(w, 32, 0.5)
     B.approx_lstm_set_launch(m, 1, 0)
     sweep(m, w, "one workgroup", 32)
+
+
+def test_anytime_rejects_bf16_models_and_bad_arguments():
+    w = synth.named("tiny")
+    say("anytime argument errors")
+    m16 = prep(w, 32, 0.5, factor_dtype=1)
+    x = torch.zeros((2, 1, 64), device="cuda")
+    h = torch.zeros((2, 1, 32), device="cuda")
+    with pytest.raises(B.ApproxLstmError) as ei:
+        B.approx_lstm_run_anytime(m16, x, 10.0, h)
+    assert ei.value.status == B.ERR_UNSUPPORTED
+    m = prep(w, 8, 0.5)
+    for dl in (0.0, -1.0):
+        with pytest.raises(B.ApproxLstmError) as ei:
+            B.approx_lstm_run_anytime(m, x, dl, h)
+        assert ei.value.status == B.ERR_INVALID_ARG
+
+
+def test_anytime_with_initial_state():
+    """h0 and c0 given: the replay starts from the same state."""
+    w = synth.named("tiny")
+    m = prep(w, 32, 0.5)
+    rng = np.random.default_rng(12)
+    h0 = rng.normal(size=(1, 32)).astype(np.float32)
+    c0 = rng.normal(size=(1, 32)).astype(np.float32)
+    x = torch.from_numpy(w.x).cuda()
+    h = torch.full((w.T, 1, 32), float("nan"), device="cuda")
+    say("anytime with initial state")
+    k, us = B.approx_lstm_run_anytime(m, x, 1e5, h, torch.from_numpy(h0).cuda(), torch.from_numpy(c0).cuda())
+    ho, _ = oracle.run_schedule(exported_factors(m), w.b, w.x, [int(v) for v in k], h0, c0)
+    assert rel_err(h.cpu().numpy(), ho) < TOL

@@ -241,3 +241,21 @@ def test_non_residual_driving_prefix():
     f = oracle.prepare(w.W, 512, 24, nz, residual=False)
     for g in range(4):
         assert np.array_equal(B.approx_lstm_get_factors(m, g)["v_idx"], f.mask[g]), g
+
+
+def test_device_factorise_and_host_only_exclude_each_other():
+    """Flag check before any device work (runs without a GPU)."""
+    w = synth.named("tiny")
+    with pytest.raises(B.ApproxLstmError) as ei:
+        prep(w, 4, p=0.5, flags=B.FLAG_HOST_ONLY | B.FLAG_DEVICE_FACTORISE)
+    assert ei.value.status == B.ERR_INVALID_ARG
+
+
+def test_host_only_model_rejects_every_run_mode():
+    """A model without a device store: run, deadline and anytime modes all
+    refuse it with INVALID_ARG, before touching a device."""
+    w = synth.named("tiny")
+    m = prep(w, 8, p=0.5)
+    for fn in ("approx_lstm_run_deadline", "approx_lstm_run_anytime"):
+        st = getattr(B.lib, fn)(m.handle, None, 2, 1, None, None, 10.0, None, None, None, None)
+        assert st == B.ERR_INVALID_ARG, fn
