@@ -525,7 +525,7 @@ def bench_batched(args, torch):
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
                 "traffic": measured_traffic("batched") if (K == 512 and abs(args.prune - 0.75) < 1e-9) else None,
-                "kernel": "one step: batched_xproj_kernel + T x (batched_hproj_kernel + batched_accum_kernel)",
+                "kernel": "one step: batched_xproj_kernel + batched_persistent_kernel (T timesteps in one launch)",
                 "flops_per_launch": flops, "algorithmic_flops_per_launch": algo,
                 "algorithmic_tflops": round(algo / (ms * 1e-3) / 1e12, 2)}
     cpu = None if args.no_cpu_baseline else cpu_baseline_batched(m, wl, K, args.cpu_seconds)

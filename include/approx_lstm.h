@@ -253,9 +253,29 @@ approx_lstm_status approx_lstm_check(approx_lstm_model* m, void* hip_stream);
  * (about 17 us more per launch); the default plain launch relies on the
  * device being otherwise idle enough to hold them, and if it is not, the
  * kernel's bounded waits expire and approx_lstm_check reports
- * APPROX_LSTM_ERR_DEVICE instead of hanging.
+ * APPROX_LSTM_ERR_DEVICE instead of hanging.  For bf16 models, blocks > 0
+ * caps the workgroups of the persistent recurrence (fewer cohorts in flight;
+ * below one cohort's workgroups the per-timestep kernels run); cooperative is
+ * ignored there.
  */
 approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks, int32_t cooperative);
+
+/*
+ * approx_lstm_set_batched_path -- kernels of a bf16 model's recurrence (Eq. (1)
+ * per gate with bf16 operands, then the Sec. II cell update), from the next
+ * run on.  persistent = 1 (the default): one persistent launch per level
+ * where the shape allows it (H and every K at most 512; sequences in cohorts
+ * of 16, each run by ceil(H/32) workgroups that exchange z and h through
+ * device memory every timestep); other shapes, and persistent = 0, run two
+ * kernels per timestep.  2 and 3 force the persistent launch's z exchange to
+ * tagged words or to flagged plain bf16 (tuning; 1 picks by the number of
+ * terms).  All compute the same products with fp32 sums; they differ only in
+ * the order of those sums.  The persistent launch relies on each cohort's
+ * workgroups being resident at once; if they are not, its bounded waits
+ * expire and approx_lstm_check reports APPROX_LSTM_ERR_DEVICE.  No effect on
+ * fp32 models.  Errors: null model, persistent outside 0..3.
+ */
+approx_lstm_status approx_lstm_set_batched_path(approx_lstm_model* m, int32_t persistent);
 
 /*
  * approx_lstm_set_timing -- enable (1) or disable (0) per-timestep device

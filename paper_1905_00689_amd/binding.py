@@ -65,6 +65,7 @@ _sigs = {
     "approx_lstm_run_anytime": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
     "approx_lstm_check": [_vp, _vp],
     "approx_lstm_set_launch": [_vp, _i32, _i32],
+    "approx_lstm_set_batched_path": [_vp, _i32],
     "approx_lstm_model_info": [_vp, ctypes.POINTER(Info)],
     "approx_lstm_set_timing": [_vp, _i32],
     "approx_lstm_get_timing": [_vp, _vp, _vp, _i32],
@@ -217,6 +218,10 @@ def approx_lstm_check(model, stream=None):
 
 def approx_lstm_set_launch(model, blocks, cooperative=0):
     return _check(lib.approx_lstm_set_launch(model.handle, int(blocks), int(cooperative)))
+
+
+def approx_lstm_set_batched_path(model, persistent):
+    return _check(lib.approx_lstm_set_batched_path(model.handle, int(persistent)))
 
 
 def approx_lstm_set_timing(model, enable):

@@ -132,12 +132,24 @@ struct approx_lstm_model {
   size_t kt_cap = 0;
   int launch_blocks = 0;             // 0 = automatic
   int cooperative = 0;               // 1: cooperative launch API
+  // persistent batched recurrence (bf16 models): cohort exchange buffers
+  int batched_persistent = 1;        // 0: per-timestep kernel pairs only; 1: persistent where it
+                                     // fits; 2, 3: persistent with z always tagged / always flagged
+  uint16_t* d_pzx = nullptr;         // [slots][G][16][Kp] bf16
+  size_t pzx_cap = 0;                // elements
+  uint16_t* d_phx = nullptr;         // [slots][16][Hp] bf16, padding columns zero
+  size_t phx_cap = 0;
+  unsigned* d_pflag = nullptr;       // [2][slots][W]
+  size_t pflag_cap = 0;
 
   ~approx_lstm_model() {
     if (!has_dev && !d_px && !d_zx && !d_hx && !d_hbx && !d_hflag && !d_err && !d_stamps && !d_stack && !d_bz &&
-        !d_bh && !d_bc && !d_kt)
+        !d_bh && !d_bc && !d_kt && !d_pzx && !d_phx && !d_pflag)
       return;
     DeviceScope ds(device);
+    dfree(d_pzx);
+    dfree(d_phx);
+    dfree(d_pflag);
     dfree(d_Vx);
     dfree(d_Vh);
     dfree(d_Ut16);
@@ -266,6 +278,59 @@ approx_lstm_status ensure_bulk(approx_lstm_model* m, size_t floats, hipStream_t 
   return APPROX_LSTM_OK;
 }
 
+// z of a persistent batched launch travel as tagged words (no flag round
+// trip, twice the bytes) up to this many terms in use (G times K rounded up
+// to 32), as plain bf16 behind flags beyond.  Measured on MI355X at the
+// batched workload (H=512, 256 sequences), the flagged form is as fast or
+// faster at every K from 32 to 512 (the tagged polls wait as long as the
+// flag round trip), so the automatic choice is always flagged.
+constexpr int kZtagTerms = 0;
+
+// Exchange buffers of the persistent batched recurrence: z and h of every
+// cohort in flight (zeroed when new, so that no stale tag can match) and the
+// flag words (zeroed when new and when the launch sequence would wrap).
+// Reserves n_levels launch sequence numbers: on return m->seq + n_levels <=
+// 0xFFFF.
+approx_lstm_status ensure_persistent(approx_lstm_model* m, size_t zx, size_t hx, size_t flags, int n_levels,
+                                     hipStream_t stream) {
+  if (!m->d_err) {
+    HIP_TRY(hipMalloc(&m->d_err, 64), "hipMalloc(err)");
+    HIP_TRY(hipMemsetAsync(m->d_err, 0, 64, stream), "hipMemsetAsync(err)");
+  }
+  approx_lstm_status st = APPROX_LSTM_OK;
+  if (round_up(zx, 4) > m->pzx_cap) {
+    st = grow(m->d_pzx, m->pzx_cap, round_up(zx, 4), stream, "hipMalloc(zx)");
+    if (st == APPROX_LSTM_OK)
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_pzx), m->pzx_cap / 4, stream),
+              "clear(zx)");
+  }
+  if (st == APPROX_LSTM_OK && round_up(hx, 4) > m->phx_cap) {
+    st = grow(m->d_phx, m->phx_cap, round_up(hx, 4), stream, "hipMalloc(hx)");
+    if (st == APPROX_LSTM_OK)
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_phx), m->phx_cap / 4, stream),
+              "clear(hx)");
+  }
+  bool clear_flags = false;
+  if (st == APPROX_LSTM_OK && round_up(flags, 2) > m->pflag_cap) {
+    st = grow(m->d_pflag, m->pflag_cap, round_up(flags, 2), stream, "hipMalloc(flags)");
+    clear_flags = true;
+  }
+  if (st != APPROX_LSTM_OK) return st;
+  if (m->seq == 0 || m->seq + (unsigned)n_levels > 0xFFFFu) {
+    clear_flags = true;
+    m->seq = 1;
+  }
+  if (clear_flags) {
+    HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_pflag), m->pflag_cap / 2, stream),
+            "clear(flags)");
+    HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_pzx), m->pzx_cap / 4, stream),
+            "clear(zx)");
+    HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_phx), m->phx_cap / 4, stream),
+            "clear(hx)");
+  }
+  return APPROX_LSTM_OK;
+}
+
 // The batched bf16 run (factor_dtype 1): arguments already checked.
 approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int B, const float* h0, const float* c0,
                                const int32_t* levels, int n_levels, float* h_out, float* c_out,
@@ -287,6 +352,18 @@ approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int 
   a.D = m->D; a.Dp = m->Dp; a.H = m->H; a.Hp = m->Hp; a.G = m->G; a.Kp = m->Kp;
   a.T = T; a.B = B; a.Bp = (int)Bp;
   a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
+  a.max_wg = std::max(1, m->launch_blocks > 0 ? std::min(m->launch_blocks, m->num_cu) : m->num_cu);
+  int W = 0, slots = 0;
+  if (m->batched_persistent && alstm::plan_batched_persistent(a, kmax, &W, &slots)) {
+    st = ensure_persistent(m, (size_t)slots * 2 * m->G * alstm::kCohort * m->Kp,
+                           (size_t)slots * 2 * alstm::kCohort * m->Hp, (size_t)slots * W, n_levels, stream);
+    if (st != APPROX_LSTM_OK) return st;
+    a.zx = m->d_pzx; a.hx = m->d_phx; a.zflag = m->d_pflag;
+    a.err = m->d_err;
+    a.ztag_terms = m->batched_persistent == 2 ? (1 << 30) : m->batched_persistent == 3 ? 0 : kZtagTerms;
+    a.tag_base = m->seq << 16;
+    m->seq += (unsigned)n_levels;
+  }
   std::vector<int> lv(levels, levels + n_levels);
   HIP_TRY(alstm::launch_batched(a, lv.data(), n_levels, stream), "launch batched kernels");
   return APPROX_LSTM_OK;
@@ -752,6 +829,14 @@ approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks, 
   if (!m || blocks < 0) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
   m->launch_blocks = blocks;
   m->cooperative = cooperative ? 1 : 0;
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_set_batched_path(approx_lstm_model* m, int32_t persistent) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (persistent < 0 || persistent > 3) return fail(APPROX_LSTM_ERR_INVALID_ARG, "persistent must be 0..3");
+  m->batched_persistent = persistent;
   return APPROX_LSTM_OK;
 }
 

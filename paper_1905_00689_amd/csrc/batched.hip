@@ -16,7 +16,7 @@
 // 4*(l/16) .. +3 of column l%16.  Every operand below is stored with the
 // contraction index contiguous, so a lane reads its 8 values as one 16-byte
 // load.
-#include "kernels.hpp"
+#include "device_common.hpp"
 
 #include <algorithm>
 
@@ -36,15 +36,6 @@ __device__ __forceinline__ f32x4 mfma(const bf16x8& a, const bf16x8& b, const f3
 __device__ __forceinline__ bf16x8 load8(const uint16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
 __device__ __forceinline__ uint16_t bf16_bits(float v) { return __builtin_bit_cast(uint16_t, (__bf16)v); }
-
-// Workgroup barrier that orders LDS traffic only: global loads still in
-// flight (prefetches) are not waited for, unlike __syncthreads, whose
-// workgroup-scope release fence waits for every outstanding memory operation.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 __device__ __forceinline__ float sigmoid_b(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 __device__ __forceinline__ float tanh_b(float x) { return 2.0f * sigmoid_b(2.0f * x) - 1.0f; }
@@ -349,6 +340,289 @@ __global__ void batched_init_kernel(BatchedArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- persistent recurrence
+// The whole recurrence of one level in one launch.  Sequences go in cohorts
+// of 16 (one MFMA tile wide); a cohort is run by W workgroups of 8 waves,
+// workgroup w owning hidden units [32w, 32w+32) of all four gates.  Every
+// wave keeps two operand slices in registers for the whole launch:
+//   * one h-projection tile: the 16 terms (g, n0 .. n0+15) of tile w*8 + wave
+//     (tiles numbered group-major, so the 4 results a lane holds are
+//     consecutive n of one group), their Vh rows over all of H;
+//   * one accumulation tile: U rows q*H + 32w + 16*(wave>>2) + (0..15) of gate
+//     q = wave & 3 over the K terms of group g(q).
+// Per timestep: z tile = sigma (P + Vh . h_{t-1}) -> bf16, published to the
+// cohort; every workgroup gathers all z of the cohort into LDS; y = U . z +
+// bias on MFMA; the cell update (one thread per (unit, sequence), c in a
+// register); h to h_out and, as bf16, published to the cohort; every
+// workgroup gathers h_t into LDS.  P of the next timestep is fetched while
+// the exchanges wait.
+// Exchanges go through device memory with agent-scope (sc1) stores and loads,
+// coherent across XCDs.  h, and z when the cohort's z are few, travel as
+// tagged 64-bit words (two bf16 values | tag << 32) that readers poll
+// directly; many z travel as plain bf16 behind one flag word per workgroup
+// (half the bytes, one more round trip).  The exchange buffers are single: a
+// workgroup writes z of step t+1 only after every workgroup has published
+// h_t, which each does after it has read all of z_t (and likewise for h).
+// Results equal the per-timestep kernels' up to the fp32 summation order of
+// each product.
+constexpr int kMaxKs = 16;   // register-resident contraction steps of 32 (H and K up to 512)
+
+// dst (LDS, row stride dld) <- src (global, row stride sld), `rows` rows of
+// 8*c8 bf16, with agent-scope (sc1) 16-byte loads, four in flight per thread
+__device__ __forceinline__ void copy_rows_coherent(uint16_t* dst, int dld, const uint16_t* src, int sld, int rows,
+                                                   int c8, int tid, int nthr) {
+  const unsigned long long addr = reinterpret_cast<unsigned long long>(src);
+  const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)addr);
+  const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(addr >> 32));
+  const int nbytes = __builtin_amdgcn_readfirstlane(rows * sld * 2);
+  uint16_t* base = reinterpret_cast<uint16_t*>(((unsigned long long)hi << 32) | lo);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(base, (short)0, nbytes, 0x00020000);
+  const int n = rows * c8;
+  for (int i0 = 0; i0 < n; i0 += 4 * nthr) {
+    u32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * nthr + tid;
+      const int r = i < n ? i / c8 : 0, c = i < n ? i - r * c8 : 0;
+      v[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (r * sld + 8 * c) * 2, 0, 16 /* sc1 */));
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * nthr + tid;
+      if (i < n) {
+        const int r = i / c8, c = i - r * c8;
+        *reinterpret_cast<u32x4*>(dst + r * dld + 8 * c) = v[u];
+      }
+    }
+  }
+}
+
+// Tagged pairs: word p of row r of src (row stride swr words) holds bf16
+// values 2p and 2p+1 of that row and the tag in its upper half.  dst (LDS, row
+// stride dld bf16) <- the values of pairs p < npairs of `rows` rows, each once
+// its word carries `tag`; up to 8 words in flight per thread, polled until
+// they arrive.  Bounded: past the spin limit, or once another wait has failed,
+// it records the failure and stores zeros.
+__device__ void gather_pairs_tagged(uint16_t* dst, int dld, const unsigned long long* src, int swr, int rows,
+                                    int npairs, unsigned tag, unsigned* err, int tid, int nthr) {
+  const int n = rows * npairs;
+  for (int base = 0; base < n; base += 8 * nthr) {
+    const unsigned long long* sp[8];
+    int dp[8];
+    unsigned pending = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = base + k * nthr + tid;
+      const int r = i < n ? i / npairs : 0, pr = i < n ? i - r * npairs : 0;
+      sp[k] = src + (size_t)r * swr + pr;
+      dp[k] = r * dld + 2 * pr;
+      if (i < n) pending |= 1u << k;
+    }
+    unsigned long long wv[8];
+    unsigned spins = 0;
+    while (pending) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if ((pending >> k) & 1u) wv[k] = load_tagged(sp[k]);
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (((pending >> k) & 1u) && (unsigned)(wv[k] >> 32) == tag) {
+          *reinterpret_cast<unsigned*>(dst + dp[k]) = (unsigned)wv[k];
+          pending &= ~(1u << k);
+        }
+      if (pending && (++spins & 255u) == 0u &&
+          (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if ((pending >> k) & 1u) *reinterpret_cast<unsigned*>(dst + dp[k]) = 0u;
+        pending = 0;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void store_coherent_u32(unsigned* p, unsigned v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void store_pair_tagged(unsigned long long* p, unsigned pair, unsigned tag) {
+  __hip_atomic_store(p, ((unsigned long long)tag << 32) | pair, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// LDS bytes of a persistent launch at Kl32 (h and z tiles, y staging)
+__host__ __device__ inline size_t persistent_lds(int G, int Hp, int Kl32) {
+  return (size_t)2 * kCohort * ((Hp + 8) + (size_t)G * (Kl32 + 8)) + sizeof(float) * 4 * 32 * 17;
+}
+
+__global__ void __launch_bounds__(512) batched_persistent_kernel(BatchedArgs a, int K, int Kl32, int level,
+                                                                 int W, int slots, int ztag) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const int slot = blockIdx.x / W, w = blockIdx.x - slot * W;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int li = lane & 15, lq = lane >> 4, lk = lq * 8;
+  const int G = a.G, H = a.H, Hp = a.Hp, Kp = a.Kp;
+  const int hld = Hp + 8, zld = Kl32 + 8;
+  uint16_t* hs = reinterpret_cast<uint16_t*>(lds_raw);                      // [16][hld]
+  uint16_t* zs = hs + kCohort * hld;                                        // [G][16][zld]
+  float* ys = reinterpret_cast<float*>(zs + (size_t)G * kCohort * zld);     // [4][32][17]
+  // a slot's exchange: z as [G*16][Kp] bf16 (flagged) or [G*16][Kp/2] tagged
+  // words; h as [16][Hp/2] tagged words
+  uint16_t* zx = a.zx + (size_t)slot * G * kCohort * Kp * 2;
+  unsigned long long* zxw = reinterpret_cast<unsigned long long*>(zx);
+  unsigned long long* hxw = reinterpret_cast<unsigned long long*>(a.hx + (size_t)slot * kCohort * Hp * 2);
+  unsigned* zflag = a.zflag + slot * W;
+  const int nkh = Hp >> 5, nku = Kl32 >> 5;
+  const int u0 = w * 32;
+  const bool exch = K > 0;   // without terms no workgroup reads another's z or h
+
+  // h-projection tile of this wave and its operands
+  const int ntn = Kl32 >> 4;
+  const int tile = w * 8 + wave;
+  const bool has_tile = tile < G * ntn;
+  const int tg = has_tile ? tile / ntn : 0, tn0 = has_tile ? (tile - tg * ntn) * 16 : 0;
+  bf16x8 va[kMaxKs];
+#pragma unroll
+  for (int ks = 0; ks < kMaxKs; ++ks) {
+    va[ks] = bf16x8{};
+    if (has_tile && ks < nkh) va[ks] = load8(a.Vh + (size_t)((tn0 + li) * G + tg) * Hp + 32 * ks + lk);
+  }
+  float sg[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int n = tn0 + 4 * lq + r;
+    sg[r] = (has_tile && n < K) ? a.sigma[n * G + tg] : 0.0f;
+  }
+  // accumulation tile of this wave
+  const int q = wave & 3, half = wave >> 2;
+  const int urow = u0 + 16 * half + li;
+  bf16x8 ua[kMaxKs];
+#pragma unroll
+  for (int ks = 0; ks < kMaxKs; ++ks) {
+    ua[ks] = bf16x8{};
+    if (urow < H && ks < nku) ua[ks] = load8(a.Ut + (size_t)(q * H + urow) * Kp + 32 * ks + lk);
+  }
+  const int zg = (G == 4) ? q : 0;
+  // cell-update role: unit u0 + (tid >> 4), sequence tid & 15 of the cohort
+  const int ul = tid >> 4, gs = tid & 15;
+  const int gu = u0 + ul;
+  const bool gu_live = gu < H;
+  const int gur = gu_live ? gu : 0;
+  const float bi = a.bias[gur], bfg = a.bias[H + gur], bgg = a.bias[2 * H + gur], bo = a.bias[3 * H + gur];
+
+  int iter = 0;
+  for (int coh = slot; coh < (a.B + kCohort - 1) / kCohort; coh += slots, ++iter) {
+    const int b0 = coh * kCohort;
+    // h_{-1}; columns past H stay zero (the h gather writes units < H only)
+    for (int i = tid; i < kCohort * Hp; i += 512) {
+      const int sq = i / Hp, k = i - sq * Hp;
+      const int b = b0 + sq;
+      const float v = (a.h0 && b < a.B && k < H) ? a.h0[(size_t)b * H + k] : 0.0f;
+      hs[sq * hld + k] = bf16_bits(v);
+    }
+    float c = 0.0f;
+    if (a.c0 && b0 + gs < a.B && gu_live) c = a.c0[(size_t)(b0 + gs) * H + gu];
+    // P of the lane's 4 result terms (sequence li), one timestep ahead
+    float pv[4] = {0.f, 0.f, 0.f, 0.f};
+    auto fetch_p = [&](int t) {
+      const float* prow = a.P + (size_t)(t * a.Bp + b0 + li) * a.pld;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int n = tn0 + 4 * lq + r;
+        pv[r] = (has_tile && n < K) ? prow[n * G + tg] : 0.0f;
+      }
+    };
+    fetch_p(0);
+    lds_barrier();
+    for (int t = 0; t < a.T; ++t) {
+      const unsigned tag = a.tag_base | (unsigned)(iter * a.T + t + 1);
+      // ---- h-projection of the wave's tile, published as bf16
+      if (has_tile) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < kMaxKs; ++ks)
+          if (ks < nkh) acc = mfma(va[ks], *reinterpret_cast<const bf16x8*>(hs + li * hld + 32 * ks + lk), acc);
+        unsigned zb[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) zb[r] = bf16_bits(sg[r] * (pv[r] + acc[r]));
+        const size_t zoff = (size_t)(tg * kCohort + li) * Kp + tn0 + 4 * lq;   // even
+        if (ztag) {
+          store_pair_tagged(zxw + zoff / 2, zb[0] | (zb[1] << 16), tag);
+          store_pair_tagged(zxw + zoff / 2 + 1, zb[2] | (zb[3] << 16), tag);
+        } else {
+          unsigned* zp = reinterpret_cast<unsigned*>(zx + zoff);
+          store_coherent_u32(zp, zb[0] | (zb[1] << 16));
+          store_coherent_u32(zp + 1, zb[2] | (zb[3] << 16));
+        }
+      }
+      if (exch) {
+        if (ztag) {
+          if (t + 1 < a.T) fetch_p(t + 1);
+          gather_pairs_tagged(zs, zld, zxw, Kp / 2, G * kCohort, Kl32 / 2, tag, a.err, tid, 512);
+        } else {
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's z stores acknowledged
+          lds_barrier();
+          if (tid == 0) __hip_atomic_store(zflag + w, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (t + 1 < a.T) fetch_p(t + 1);
+          await_flags(zflag, W, tag, a.err, tid, 512);
+          lds_barrier();
+          copy_rows_coherent(zs, zld, zx, Kp, G * kCohort, Kl32 >> 3, tid, 512);
+        }
+      } else if (t + 1 < a.T) {
+        fetch_p(t + 1);
+      }
+      lds_barrier();
+      // ---- y = U . z for the wave's rows
+      {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < kMaxKs; ++ks)
+          if (ks < nku)
+            acc = mfma(ua[ks], *reinterpret_cast<const bf16x8*>(zs + (zg * kCohort + li) * zld + 32 * ks + lk), acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ys[(q * 32 + 16 * half + 4 * lq + r) * 17 + li] = acc[r];
+      }
+      lds_barrier();
+      // ---- gates and cell update
+      const float yi = ys[(0 * 32 + ul) * 17 + gs] + bi;
+      const float yf = ys[(1 * 32 + ul) * 17 + gs] + bfg;
+      const float yg = ys[(2 * 32 + ul) * 17 + gs] + bgg;
+      const float yo = ys[(3 * 32 + ul) * 17 + gs] + bo;
+      c = sigmoid_b(yf) * c + sigmoid_b(yi) * tanh_b(yg);
+      const float h = sigmoid_b(yo) * tanh_b(c);
+      const int b = b0 + gs;
+      if (gu_live && b < a.B) {
+        a.h_out[(((size_t)level * a.T + t) * a.B + b) * H + gu] = h;
+        if (a.c_out && t == a.T - 1) a.c_out[((size_t)level * a.B + b) * H + gu] = c;
+      }
+      if (exch) {
+        // units in pairs (lanes l and l+16 hold units 2m and 2m+1 of one
+        // sequence); a unit past H travels as zero
+        const unsigned hb = gu_live ? (unsigned)bf16_bits(h) : 0u;
+        const unsigned hn = (unsigned)__shfl_down((int)hb, 16, 64);
+        if ((lq & 1) == 0 && gu_live) store_pair_tagged(hxw + ((size_t)gs * Hp + gu) / 2, hb | (hn << 16), tag);
+        gather_pairs_tagged(hs, hld, hxw, Hp / 2, kCohort, (H + 1) / 2, tag, a.err, tid, 512);
+      }
+      lds_barrier();
+    }
+  }
+}
+
+int plan_batched_persistent(const BatchedArgs& a, int K, int* W, int* slots) {
+  const int Kl32 = ((K + 31) / 32) * 32;
+  const int w = (a.H + 31) / 32;
+  const int ncoh = (a.B + kCohort - 1) / kCohort;
+  if (a.Hp > 32 * kMaxKs || Kl32 > 32 * kMaxKs || a.G * (Kl32 / 16) > 8 * w) return 0;
+  if (w > a.max_wg || a.Bp % kCohort != 0) return 0;
+  if (persistent_lds(a.G, a.Hp, Kl32) > kLdsCap) return 0;
+  const int s = std::max(1, std::min(ncoh, a.max_wg / w));
+  const long long iters = (ncoh + s - 1) / s;
+  if (iters * a.T >= 65535) return 0;
+  *W = w;
+  *slots = s;
+  return 1;
+}
+
 hipError_t launch_batched(const BatchedArgs& a, const int* levels, int n_levels, hipStream_t stream) {
   if (a.Bp % kBatchAlign != 0 || a.Bp < a.B || a.Bp > (1 << 20) || a.Dp % kPanelDAlign != 0 || a.Dp < a.D ||
       a.Hp % 32 != 0 || a.Hp < a.H || a.Kp % 32 != 0)
@@ -373,6 +647,16 @@ hipError_t launch_batched(const BatchedArgs& a, const int* levels, int n_levels,
     const int K = levels[l];
     const int Kl32 = ((K + 31) / 32) * 32;
     p.rows = a.G * Kl32;
+    int W = 0, slots = 0;
+    if (a.zx && a.hx && a.zflag && a.err && plan_batched_persistent(p, K, &W, &slots)) {
+      // one launch sequence number per level: its tags differ from every earlier launch's
+      p.tag_base = a.tag_base + ((unsigned)l << 16);
+      const int ztag = (a.G * Kl32 <= a.ztag_terms) ? 1 : 0;
+      batched_persistent_kernel<<<dim3(W * slots), dim3(512), persistent_lds(a.G, a.Hp, Kl32), stream>>>(
+          p, K, Kl32, l, W, slots, ztag);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      continue;
+    }
     if (init) {
       batched_init_kernel<<<dim3(128), dim3(256), 0, stream>>>(p);
       if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -164,7 +164,29 @@ struct BatchedArgs {
   int rows;        // panel rows a launch covers (set per launch)
   int pld;         // row count of P: G * (largest level rounded up to 32)
   int xvec;        // 1: x rows may be read as 16-byte vectors (D % 4 == 0, x 16-byte aligned)
+  // persistent recurrence (one launch per level instead of T kernel pairs);
+  // null zx selects the per-timestep kernels
+  uint16_t* zx;      // [slots][2*G*16*Kp] bf16 slots: z of a cohort's current timestep, as
+                     // [G*16][Kp] bf16 behind flags or [G*16][Kp/2] tagged 64-bit words
+  uint16_t* hx;      // [slots][2*16*Hp]: h of a cohort's current timestep, [16][Hp/2] tagged words
+  unsigned* zflag;   // [slots][W]: workgroup w's tag once its (untagged) z tile is stored
+  unsigned* err;     // set when a bounded wait expires
+  unsigned tag_base; // launch sequence << 16 of level 0; level l uses tag_base + (l << 16)
+  int max_wg;        // workgroups that may be resident at once (one per compute unit)
+  int ztag_terms;    // z travel as tagged words when G * K (rounded up to 32) <= this
 };
+
+// Sequences per cohort of the persistent batched recurrence (the MFMA tile width).
+constexpr int kCohort = 16;
+
+// Shape of a persistent batched launch at budget K: W workgroups per cohort
+// (32 hidden units each), `slots` cohorts in flight.  Returns 0 when the
+// shape does not fit (then the per-timestep kernels run): H and K each at
+// most 512 (their contraction steps are held in registers), at most one
+// h-projection tile of 16 terms per wave, a cohort's workgroups resident at
+// once, and fewer than 2^16 tagged timesteps per launch.  Exchange sizes (in
+// 16-bit elements): zx slots*2*G*16*Kp, hx slots*2*16*Hp; flags slots*W.
+int plan_batched_persistent(const BatchedArgs& a, int K, int* W, int* slots);
 
 // Exact (dense) LSTM: x [T][B][D], h0, c0 [B][H] or null, h_out [T][B][H],
 // c_out [B][H] or null; Wx [4H][D], Wh [4H][H], bias [4H] (gate rows i, f,
@@ -199,8 +221,8 @@ size_t plan_exact(ExactArgs& a, int P);
 hipError_t launch_exact(const ExactArgs& a, int blocks, hipStream_t stream);
 
 // Launches, on `stream`, the x-projection once and then, for every level,
-// T pairs of per-timestep kernels.  Requires Bp % 64 == 0 and every level
-// K <= Kp.
+// either the persistent recurrence (a.zx set and the shape fits) or T pairs
+// of per-timestep kernels.  Requires Bp % 64 == 0 and every level K <= Kp.
 hipError_t launch_batched(const BatchedArgs& a, const int* levels, int n_levels, hipStream_t stream);
 
 }  // namespace alstm

@@ -177,3 +177,57 @@ def test_batched_full_size_sampled_sequences(full):
     pick = np.random.default_rng(3).choice(256, size=12, replace=False)
     ho, _ = oracle.run(f, w.b, w.x[:, pick], levels, operand_round="bf16")
     check_levels(h[:, :, pick], ho, levels)
+
+
+# ------------------------------------------- persistent vs per-timestep kernels
+def test_batched_persistent_and_per_timestep_paths_agree(quarter):
+    """The quarter-size workload through the persistent recurrence (cohorts of
+    16 sequences over 4 workgroups each, z and h exchanged through device
+    memory) and through the per-timestep kernel pair: both within the bar of
+    the oracle on the exported terms, and close to each other (they differ
+    only in the fp32 summation order of the two products)."""
+    w, m = quarter
+    levels = [0, 9, 64, 128]
+    say("batched quarter: persistent vs per-timestep kernels", levels)
+    f = exported_factors(m)
+    ho, _ = oracle.run(f, w.b, w.x, levels, operand_round="bf16")
+    try:
+        B.approx_lstm_set_batched_path(m, 0)
+        h_pair, _ = run_gpu(m, w.x, levels)
+    finally:
+        B.approx_lstm_set_batched_path(m, 1)
+    check_levels(h_pair, ho, levels)
+    runs = {}
+    for mode in (1, 2, 3):   # automatic, z as tagged words, z behind flags
+        try:
+            B.approx_lstm_set_batched_path(m, mode)
+            runs[mode], _ = run_gpu(m, w.x, levels)
+        finally:
+            B.approx_lstm_set_batched_path(m, 1)
+        say("  persistent mode", mode)
+        check_levels(runs[mode], ho, levels)
+        for j in range(len(levels)):
+            assert rel_err(runs[mode][j], h_pair[j]) < TOL
+    # the z exchange's form changes no arithmetic
+    assert np.array_equal(runs[2], runs[3])
+    assert np.array_equal(runs[1], runs[2])
+
+
+@pytest.mark.parametrize("blocks", [4, 8])
+def test_batched_persistent_cohorts_in_turn(quarter, blocks):
+    """4 cohorts of 16 sequences on one or two cohorts' worth of workgroups:
+    each workgroup runs several cohorts in turn, reusing the exchange buffers
+    with fresh tags; bitwise equal to the run with every cohort in flight."""
+    w, m = quarter
+    levels = [0, 40, 128]
+    say("batched quarter persistent, workgroup cap", blocks)
+    wide, _ = run_gpu(m, w.x, levels)
+    try:
+        B.approx_lstm_set_launch(m, blocks)
+        narrow, _ = run_gpu(m, w.x, levels)
+        again, _ = run_gpu(m, w.x, levels)
+    finally:
+        B.approx_lstm_set_launch(m, 0)
+    assert np.array_equal(wide, narrow)
+    assert np.array_equal(wide, again)
+    B.approx_lstm_check(m)
