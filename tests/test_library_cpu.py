@@ -259,3 +259,15 @@ def test_host_only_model_rejects_every_run_mode():
     for fn in ("approx_lstm_run_deadline", "approx_lstm_run_anytime"):
         st = getattr(B.lib, fn)(m.handle, None, 2, 1, None, None, 10.0, None, None, None, None)
         assert st == B.ERR_INVALID_ARG, fn
+
+
+def test_batched_path_selector_arguments():
+    """approx_lstm_set_batched_path accepts 0..3 and refuses anything else or a
+    null model (a setting only: no device work)."""
+    w = synth.named("tiny")
+    m = prep(w, 4, p=0.5)
+    for mode in (0, 1, 2, 3, 1):
+        assert B.lib.approx_lstm_set_batched_path(m.handle, mode) == B.OK
+    for mode in (-1, 4):
+        assert B.lib.approx_lstm_set_batched_path(m.handle, mode) == B.ERR_INVALID_ARG
+    assert B.lib.approx_lstm_set_batched_path(None, 1) == B.ERR_INVALID_ARG
