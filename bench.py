@@ -46,12 +46,14 @@ def main():
     ap.add_argument("--prune", type=float, default=0.75)
     ap.add_argument("--K", type=int, default=512)
     ap.add_argument("--blocks", type=int, default=0, help="workgroups of the run kernel (0 = automatic)")
-    ap.add_argument("--sweep", default="1,2,4,8,16,32,64,128,256,512")
+    ap.add_argument("--sweep", default="0,1,2,4,8,16,32,64,128,256,512")
     ap.add_argument("--sweep-steps", type=int, default=50)
     ap.add_argument("--blocks-sweep", default="", help="comma list of workgroup counts to time at K (tuning)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-phases", action="store_true", help="skip the in-kernel phase stamps")
     ap.add_argument("--no-anytime", action="store_true", help="skip the error-vs-time comparison with the row-tile baseline")
+    ap.add_argument("--no-batched", action="store_true",
+                    help="skip the batched (256 sequences, bf16 MFMA) summary in the default line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only time a plain 256 MiB device copy (reference for HBM counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -192,6 +194,7 @@ def main():
     exact = {"us_per_timestep": round(ms_exact * 1e3 / T, 4), "timesteps_per_s": round(T * Bn / (ms_exact * 1e-3), 1),
              "weights_bytes": 4 * 4 * H * (D + H)}
     anytime = None if args.no_anytime else anytime_comparison(torch, B, stream)
+    batched = None if args.no_batched else batched_summary(args, torch)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -207,7 +210,7 @@ def main():
                    "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
         "us_per_timestep": round(us_per_ts, 4), "step_ms": dist, "prepare_s": round(prep_s, 2),
         "phases": phases, "sweep": sweep, "tune": tune, "exact_baseline": exact, "anytime": anytime,
-        "roofline": roofline, "cpu_baseline": cpu,
+        "batched": batched, "roofline": roofline, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 
@@ -472,7 +475,19 @@ def mfma_flops_batched(G, D, H, T, Bp, K):
     return xproj + T * (hproj + accum)
 
 
-def bench_batched(args, torch):
+def batched_summary(args, torch):
+    """The batched workload's sweep (us per timestep and MFMA fraction at each
+    budget) and its K=512 roofline, for the default line; the full record is
+    `--workload batched`."""
+    sub = argparse.Namespace(**vars(args))
+    sub.K, sub.steps, sub.warmup, sub.prune, sub.no_cpu_baseline = 512, 30, 5, 0.75, True
+    sub.sweep_steps = 30
+    out = bench_batched(sub, torch, emit=False, step_dist=False)
+    return {"workload": out["config"]["workload"], "us_per_timestep": out["us_per_timestep"],
+            "timesteps_per_s": out["value"], "sweep": out["sweep"], "roofline": out["roofline"]}
+
+
+def bench_batched(args, torch, emit=True, step_dist=True):
     """The batched workload: 256 independent driving-shaped sequences (D=2048,
     H=512, T=16), rank 512, 75% pruning, bf16 factors with fp32 accumulation
     on MFMA.  A step is one approx_lstm_run over the batch at budget K."""
@@ -510,7 +525,8 @@ def bench_batched(args, torch):
 
     K = args.K
     ms = timed(K, args.steps, args.warmup)
-    dist = step_distribution(torch, lambda: B.approx_lstm_run(m, x, [K], h_out, stream=stream), stream, args.steps)
+    dist = (step_distribution(torch, lambda: B.approx_lstm_run(m, x, [K], h_out, stream=stream), stream, args.steps)
+            if step_dist else None)
     sweep = {"K": [], "us_per_timestep": [], "timesteps_per_s": [], "mfma_frac": []}
     for k in [int(v) for v in args.batched_sweep.split(",") if v]:
         msk = timed(k, args.sweep_steps, 5)
@@ -540,7 +556,9 @@ def bench_batched(args, torch):
         "us_per_timestep": round(ms * 1e3 / T, 4), "step_ms": dist, "prepare_s": round(prep_s, 2),
         "sweep": sweep, "roofline": roofline, "cpu_baseline": cpu,
     }
-    print(json.dumps(out), flush=True)
+    if emit:
+        print(json.dumps(out), flush=True)
+    return out
 
 
 def cpu_baseline_batched(m, wl, K, seconds):
