@@ -388,6 +388,10 @@ int auto_blocks(const approx_lstm_model* m, int GK, int LB, int LB_seq) {
     const int rows_max = std::max(1, alstm::kThreads / (4 * S));
     want = std::max(want, (m->H + rows_max - 1) / rows_max);
   }
+  // one sequence with 32 to 127 terms per group: 16 workgroups beat the 4 to
+  // 15 above (MI355X, driving shape, one box: K = 32 5.62 against 5.72 us per
+  // timestep, K = 64 5.74 against 6.06; K = 16 stays fastest on 4)
+  if (LB_seq == 1 && m->G > 0 && GK / m->G >= 32 && GK / m->G < 128) want = std::max(want, 16);
   return std::max(1, std::min(cap, want));
 }
 

@@ -177,6 +177,14 @@ def test_batched_full_size_sampled_sequences(full):
     pick = np.random.default_rng(3).choice(256, size=12, replace=False)
     ho, _ = oracle.run(f, w.b, w.x[:, pick], levels, operand_round="bf16")
     check_levels(h[:, :, pick], ho, levels)
+    # the per-timestep kernel pair at the same size (the persistent launch is the default)
+    try:
+        B.approx_lstm_set_batched_path(m, 0)
+        hp, _ = run_gpu(m, w.x, levels)
+    finally:
+        B.approx_lstm_set_batched_path(m, 1)
+    say("  per-timestep kernels")
+    check_levels(hp[:, :, pick], ho, levels)
 
 
 # ------------------------------------------- persistent vs per-timestep kernels
