@@ -169,6 +169,13 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
 
   // phase-A lane roles: 16 lanes per term, 4 terms per wave per pass
   const int sub = lane >> 4, sla = lane & 15;
+  // per-level budget and phase-B lane count, level l in lane l of one
+  // register each, read with v_readlane: opaque to the compiler, so that it
+  // keeps them instead of reloading them from the kernel arguments (a scalar
+  // memory round trip) in every pass over the (level, sequence) pairs
+  int vlev = lane < kMaxLevels ? a.levels[lane] : 0;
+  int vlanes = lane < kMaxLevels ? a.lanes_b[lane] : 1;
+  asm volatile("" : "+v"(vlev), "+v"(vlanes));
   // phase-B thread roles (register path: one output row per S threads)
   const int S0 = a.lanes_b[0];
   const int ob = threadIdx.x / S0, slb = threadIdx.x % S0;
@@ -300,7 +307,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     // ---- phase A: z = sigma * (P_x + prune(v)_h . h_{t-1}) for the owned terms ----
     for (int lb = 0; lb < LB; ++lb) {
       const int l = lb / B, b = lb % B;
-      const int GKl = G * (ONLINE ? kcur : a.levels[l]);
+      const int GKl = G * (ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l));
       const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
       const float* h = hs + lb * H;
       if constexpr (HPL > 0) {
@@ -343,7 +350,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     if (stamp) a.stamps[3 + 4 * t] = clock64();
     if (publisher && !local) {
       for (int lb = 0; lb < LB; ++lb) {
-        const int GKl = G * (ONLINE ? kcur : a.levels[lb / B]);
+        const int GKl = G * (ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, lb / B));
         const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
         for (int i = lane; i < nl; i += 64)
           publish(a.zx + (size_t)lb * P * OM + j * OM + i, zown[lb * OM + i], tag);
@@ -354,7 +361,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     if (rc > 0) {
       for (int lb = 0; lb < LB; ++lb) {
         const int l = lb / B;
-        const int Kl = ONLINE ? kcur : a.levels[l];
+        const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l);
         if (!local && !publisher) {
           // P_x of the next timestep travels while the z words are awaited
           if (!a.px_all && lb == 0 && t + 1 < T) {
@@ -394,7 +401,9 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
             if (yslot[o] >= 0 && slb == 0) ys[yslot[o]] = acc + bs[yslot[o]];
           }
         } else {
-          const int S = a.lanes_b[l], OPP = kThreads / S, os = threadIdx.x / S, sl = threadIdx.x % S;
+          // S is a power of two (1 .. 16)
+          const int S = __builtin_amdgcn_readlane(vlanes, l), lgS = 31 - __builtin_clz(S);
+          const int OPP = kThreads >> lgS, os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
           for (int base = 0; base < outs; base += OPP) {
             const int ol = base + os;
             float acc = 0.0f;
