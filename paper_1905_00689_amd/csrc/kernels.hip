@@ -358,7 +358,24 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     }
 
     // ---- phase B: y = b + sum_n z_n u_n for the owned rows, gates, c and h ----
-    if (rc > 0) {
+    if (!ONLINE && GK == 0 && rc > 0) {
+      // every level at K = 0: y is the bias alone (the same values as 0 + b
+      // below), so all (level, sequence) pairs take one pass and one barrier
+      if (stamp) a.stamps[4 + 4 * t] = clock64();
+      for (int i = threadIdx.x; i < LB * rc; i += kThreads) {
+        const int lb = i / rc, rr = i - lb * rc;
+        const float gi = sigmoid_fast(bs[0 * RP + rr]);
+        const float gf = sigmoid_fast(bs[1 * RP + rr]);
+        const float gg = tanh_fast(bs[2 * RP + rr]);
+        const float go = sigmoid_fast(bs[3 * RP + rr]);
+        const float c = gf * cs[lb * RP + rr] + gi * gg;
+        const float hv2 = go * tanh_fast(c);
+        cs[lb * RP + rr] = c;
+        hown[lb * RP + rr] = hv2;
+        if (local) hs[lb * H + r0 + rr] = hv2;
+      }
+      lds_barrier();
+    } else if (rc > 0) {
       for (int lb = 0; lb < LB; ++lb) {
         const int l = lb / B;
         const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l);

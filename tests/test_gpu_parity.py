@@ -178,6 +178,30 @@ def test_zero_budget_spreads_over_workgroups():
             assert np.array_equal(h, ref), P
 
 
+@pytest.mark.parametrize("init", [False, True])
+def test_zero_budget_single_pass_equals_general_path(init):
+    """A run whose every level has K = 0 takes phase B in one pass over all
+    (level, sequence) pairs; a K = 0 level next to a positive budget takes
+    the general pass per pair.  Both give the same bits (y is the bias
+    alone), with and without an initial state, and equal the oracle."""
+    w = synth.make(64, 32, 6, 5, index=17, xkind="normal")
+    m = prep(w, 8, 0.5)
+    h0 = c0 = None
+    if init:
+        rng = np.random.default_rng(5)
+        h0 = rng.normal(size=(5, 32)).astype(np.float32)
+        c0 = rng.normal(size=(5, 32)).astype(np.float32)
+    say("K = 0 single pass vs general path, initial state", init)
+    hz, cz = run_gpu(m, w.x, [0, 0], h0, c0, want_c=True)
+    hm, cm = run_gpu(m, w.x, [0, 5], h0, c0, want_c=True)
+    for j in range(2):
+        assert np.array_equal(hz[j], hm[0]), j
+        assert np.array_equal(cz[j], cm[0]), j
+    ho, co = oracle.run(oracle.prepare(w.W, 32, 8, 48), w.b, w.x, [0], h0, c0)
+    assert rel_err(hz[0], ho[0]) < TOL
+    assert np.abs(cz[0] - co[0]).max() < TOL * max(1.0, np.abs(co[0]).max())
+
+
 def test_driving_full_rank_without_pruning_is_the_exact_lstm(driving):
     say("driving p=0 rank 512 vs exact LSTM")
     m = prep(driving, 512, 0.0)
