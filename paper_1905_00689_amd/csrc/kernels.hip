@@ -97,6 +97,72 @@ __device__ __forceinline__ void gather_level_any(float* zs, const uint16_t* slot
   else gather_level<8>(zs, slot_term, src, nslots, GKl, G, Kmax, tag, err, tid, nthr);
 }
 
+// z gather of every (level, sequence) pair at once: word i of the LB x nslots
+// exchange words belongs to pair lb = i / nslots, slot s = i % nslots, which
+// carries term tau = slot_term[s]; it lands at zs[lb*GK + g*Kmax + n] (tau =
+// n*G + g) when tau is inside the budget of the pair's level (lane l of vlev
+// holds level l's budget; kcur >= 0 overrides it).  One polling pipeline for
+// all pairs, the same two-generation polling as gather_level.
+template <int NS>
+__device__ void gather_every_pair(float* zs, const uint16_t* slot_term, const unsigned long long* src, int nslots,
+                                  int LB, int B, int GK, int G, int Kmax, int vlev, int kcur, unsigned tag,
+                                  unsigned* err, int tid, int nthr) {
+  const int n = LB * nslots;
+  for (int base = 0; base < n; base += nthr * NS) {
+    const unsigned long long* sp[NS];
+    int dst[NS];
+    unsigned pending = 0;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      const int i = base + k * nthr + tid;
+      const int lb = i < n ? i / nslots : 0, s = i < n ? i - lb * nslots : 0;
+      const int lev = __shfl(vlev, lb / B, 64);
+      const int GKl = G * (kcur >= 0 ? kcur : lev);
+      const int tau = i < n ? (int)slot_term[s] : GKl;
+      sp[k] = src + (i < n ? i : 0);
+      dst[k] = lb * GK + ((G == 4) ? ((tau & 3) * Kmax + (tau >> 2)) : tau);
+      if (tau < GKl) pending |= 1u << k;
+    }
+    if (!pending) continue;
+    unsigned long long wa[NS], wb[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) wa[k] = load_tagged(sp[k]);
+    __builtin_amdgcn_s_sleep(4);
+#pragma unroll
+    for (int k = 0; k < NS; ++k) wb[k] = load_tagged(sp[k]);
+    unsigned spins = 0;
+    while (true) {
+#pragma unroll
+      for (int k = 0; k < NS; ++k)
+        if (((pending >> k) & 1u) && (unsigned)(wa[k] >> 32) == tag) {
+          zs[dst[k]] = __uint_as_float((unsigned)wa[k]);
+          pending &= ~(1u << k);
+        }
+      if (!pending) break;
+#pragma unroll
+      for (int k = 0; k < NS; ++k) wa[k] = load_tagged(sp[k]);
+#pragma unroll
+      for (int k = 0; k < NS; ++k)
+        if (((pending >> k) & 1u) && (unsigned)(wb[k] >> 32) == tag) {
+          zs[dst[k]] = __uint_as_float((unsigned)wb[k]);
+          pending &= ~(1u << k);
+        }
+      if (!pending) break;
+#pragma unroll
+      for (int k = 0; k < NS; ++k) wb[k] = load_tagged(sp[k]);
+      spins += 2;
+      if ((spins & 254u) == 0u &&
+          (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int k = 0; k < NS; ++k)
+          if ((pending >> k) & 1u) zs[dst[k]] = 0.0f;
+        break;
+      }
+    }
+  }
+}
+
 // LDS carve-up shared by the host planner and the kernel (byte offsets).
 struct Layout {
   size_t zs, hs, ys, bs, cs, zown, hown, sig, pxb, zmap, hval, hidx, us, total;
@@ -110,10 +176,10 @@ __host__ __device__ inline Layout layout_of(const RunArgs& a, int online) {
   const size_t kmax = a.G > 0 ? (size_t)a.GK / a.G : 0;
   size_t o = 0;
   // z of one (level, seq), [g][Kmax]; a single workgroup keeps every pair's
-  l.zs = o;     o = align16(o + 4 * (a.P == 1 ? LB : 1) * (a.GK > 1 ? (size_t)a.GK : 1));
+  l.zs = o;     o = align16(o + 4 * ((a.P == 1 || a.allpairs) ? LB : 1) * (a.GK > 1 ? (size_t)a.GK : 1));
   // h_{t-1} per (level, seq); an online run receives K_t in one more slot
   l.hs = o;     o = align16(o + 4 * (LB * a.H + (online ? 1 : 0)));
-  l.ys = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // y of the owned rows
+  l.ys = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per * (a.allpairs ? LB : 1));   // y of the owned rows
   l.bs = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // bias of the owned rows
   l.cs = o;     o = align16(o + 4 * LB * a.rows_per);                 // c of the owned rows
   l.zown = o;   o = align16(o + 4 * LB * (size_t)a.owned_max);        // z of the owned terms
@@ -139,7 +205,7 @@ __host__ __device__ inline Layout layout_of(const RunArgs& a, int online) {
 // 4*rows_per*S <= 512*OPT); 0: U rows in LDS (ustride > 0) or from global.
 // ONLINE: one level whose budget is chosen per timestep (RunArgs::online);
 // the fixed-budget kernels carry none of its code.
-template <int HPL, int OPT, int UPT, bool ONLINE>
+template <int HPL, int OPT, int UPT, bool ONLINE, bool AP>
 __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   const Layout L = layout_of(a, ONLINE ? 1 : 0);
@@ -200,6 +266,9 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     const int tb = i / n_owned, io = i - tb * n_owned;
     pxb[tb * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + tb];
   }
+  // z of every pair held here start at zero: a level at K = 0 never writes
+  // its z, and the register accumulation multiplies them by zero
+  for (int i = threadIdx.x; i < ((P == 1 || a.allpairs) ? LB : 1) * GK; i += kThreads) zs[i] = 0.0f;
   // exchange slot s = j'*OM + i' carries term tau = j' + i'*P
   for (int sl = threadIdx.x; sl < P * OM; sl += kThreads) {
     const int jj = sl / OM, ii = sl - jj * OM;
@@ -376,86 +445,187 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
       }
       lds_barrier();
     } else if (rc > 0) {
-      for (int lb = 0; lb < LB; ++lb) {
-        const int l = lb / B;
-        const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l);
-        if (!local && !publisher) {
-          // P_x of the next timestep travels while the z words are awaited
-          if (!a.px_all && lb == 0 && t + 1 < T) {
+      if constexpr (AP) {
+        // every pair at once: one gather of all their z, one accumulation
+        // pass, one cell-update pass.
+        // The x-part projections of the next timestep travel while z is awaited.
+        auto prefetch_px = [&]() {
+          if (!a.px_all && t + 1 < T) {
             float* pxn = pxb + ((t + 1) & 1) * B * OM;
             for (int i = threadIdx.x; i < B * n_owned; i += gthr) {
               const int b = i / n_owned, io = i - b * n_owned;
               pxn[b * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + (t + 1) * B + b];
             }
           }
-          // every slot of the exchange whose term is in this level (slots of
-          // workgroups that own fewer terms are skipped by the map check)
-          const int nslots = P * OM;
-          const int GKl = G * Kl;
-          gather_level_any(zs, zmap, a.zx + (size_t)lb * P * OM, nslots, GKl, G, Kmax, tag, a.err, threadIdx.x, gthr);
-        }
-        lds_barrier();
-        if (stamp && lb == 0) a.stamps[4 + 4 * t] = clock64();
-        const float* zl = zs + (local ? lb * GK : 0);
-        if constexpr (UPT > 0) {
-          // branch-free: entries past the budget multiply a valid z by 0
+        };
+        // y of the owned rows of one pair: yl[q*RP + rr] = b + sum_{n<Kl} u z
+        auto accumulate = [&](const float* zl, float* yl, int Kl, int l) {
+          if constexpr (UPT > 0) {
+            // branch-free: entries past the budget multiply a valid z by 0
 #pragma unroll
-          for (int o = 0; o < OPT; ++o) {
-            // all z reads first (independent LDS loads in flight), then the FMAs
-            float zv[UPT];
+            for (int o = 0; o < OPT; ++o) {
+              // all z reads first (independent LDS loads in flight), then the FMAs
+              float zv[UPT];
 #pragma unroll
-            for (int k = 0; k < UPT; ++k) {
-              const int n = slb + S0 * k;
-              zv[k] = zl[zbase[o] + (n < Kl ? n : 0)];
-            }
-            float acc = 0.0f;
-#pragma unroll
-            for (int k = 0; k < UPT; ++k) {
-              const int n = slb + S0 * k;
-              acc += (n < Kl ? uv[o * UPT + k] : 0.0f) * zv[k];
-            }
-            acc = group_sum_rt(acc, S0);
-            if (yslot[o] >= 0 && slb == 0) ys[yslot[o]] = acc + bs[yslot[o]];
-          }
-        } else {
-          // S is a power of two (1 .. 16)
-          const int S = __builtin_amdgcn_readlane(vlanes, l), lgS = 31 - __builtin_clz(S);
-          const int OPP = kThreads >> lgS, os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
-          for (int base = 0; base < outs; base += OPP) {
-            const int ol = base + os;
-            float acc = 0.0f;
-            int q = 0, rr = 0;
-            if (ol < outs) {
-              q = ol / rc;
-              rr = ol - q * rc;
-              const float* zg = zl + ((G == 4) ? q : 0) * Kmax;
-              if (a.ustride) {
-                const float* urow = us + (size_t)(q * RP + rr) * a.ustride;
-#pragma unroll 8
-                for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
-              } else {
-                const float* urow = a.Ut + (size_t)(q * H + r0 + rr) * N;
-#pragma unroll 8
-                for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+              for (int k = 0; k < UPT; ++k) {
+                const int n = slb + S0 * k;
+                zv[k] = zl[zbase[o] + (n < Kl ? n : 0)];
               }
+              float acc = 0.0f;
+#pragma unroll
+              for (int k = 0; k < UPT; ++k) {
+                const int n = slb + S0 * k;
+                acc += (n < Kl ? uv[o * UPT + k] : 0.0f) * zv[k];
+              }
+              acc = group_sum_rt(acc, S0);
+              if (yslot[o] >= 0 && slb == 0) yl[yslot[o]] = acc + bs[yslot[o]];
             }
-            acc = group_sum_rt(acc, S);
-            if (sl == 0 && ol < outs) ys[q * RP + rr] = acc + bs[q * RP + rr];
+          } else {
+            // S is a power of two (1 .. 16)
+            const int S = __builtin_amdgcn_readlane(vlanes, l), lgS = 31 - __builtin_clz(S);
+            const int OPP = kThreads >> lgS, os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
+            for (int base = 0; base < outs; base += OPP) {
+              const int ol = base + os;
+              float acc = 0.0f;
+              int q = 0, rr = 0;
+              if (ol < outs) {
+                q = ol / rc;
+                rr = ol - q * rc;
+                const float* zg = zl + ((G == 4) ? q : 0) * Kmax;
+                if (a.ustride) {
+                  const float* urow = us + (size_t)(q * RP + rr) * a.ustride;
+#pragma unroll 8
+                  for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+                } else {
+                  const float* urow = a.Ut + (size_t)(q * H + r0 + rr) * N;
+#pragma unroll 8
+                  for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+                }
+              }
+              acc = group_sum_rt(acc, S);
+              if (sl == 0 && ol < outs) yl[q * RP + rr] = acc + bs[q * RP + rr];
+            }
           }
-        }
-        lds_barrier();
-        for (int rr = threadIdx.x; rr < rc; rr += kThreads) {
-          const float gi = sigmoid_fast(ys[0 * RP + rr]);
-          const float gf = sigmoid_fast(ys[1 * RP + rr]);
-          const float gg = tanh_fast(ys[2 * RP + rr]);
-          const float go = sigmoid_fast(ys[3 * RP + rr]);
+        };
+        // gates and the c/h update of owned unit rr of pair lb
+        auto cell = [&](const float* yl, int lb, int rr) {
+          const float gi = sigmoid_fast(yl[0 * RP + rr]);
+          const float gf = sigmoid_fast(yl[1 * RP + rr]);
+          const float gg = tanh_fast(yl[2 * RP + rr]);
+          const float go = sigmoid_fast(yl[3 * RP + rr]);
           const float c = gf * cs[lb * RP + rr] + gi * gg;
           const float hv2 = go * tanh_fast(c);
           cs[lb * RP + rr] = c;
           hown[lb * RP + rr] = hv2;
           if (local) hs[lb * H + r0 + rr] = hv2;
+        };
+        if (!local && !publisher) {
+          prefetch_px();
+          const int nslots = P * OM, n = LB * nslots, per = (n + gthr - 1) / gthr;
+          const int kc = ONLINE ? kcur : -1;
+          if (per <= 1)
+            gather_every_pair<1>(zs, zmap, a.zx, nslots, LB, B, GK, G, Kmax, vlev, kc, tag, a.err, threadIdx.x, gthr);
+          else if (per <= 2)
+            gather_every_pair<2>(zs, zmap, a.zx, nslots, LB, B, GK, G, Kmax, vlev, kc, tag, a.err, threadIdx.x, gthr);
+          else if (per <= 3)
+            gather_every_pair<3>(zs, zmap, a.zx, nslots, LB, B, GK, G, Kmax, vlev, kc, tag, a.err, threadIdx.x, gthr);
+          else if (per <= 5)
+            gather_every_pair<5>(zs, zmap, a.zx, nslots, LB, B, GK, G, Kmax, vlev, kc, tag, a.err, threadIdx.x, gthr);
+          else
+            gather_every_pair<8>(zs, zmap, a.zx, nslots, LB, B, GK, G, Kmax, vlev, kc, tag, a.err, threadIdx.x, gthr);
         }
         lds_barrier();
+        if (stamp) a.stamps[4 + 4 * t] = clock64();
+        for (int lb = 0; lb < LB; ++lb)
+          accumulate(zs + lb * GK, ys + lb * 4 * RP, ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, lb / B), lb / B);
+        lds_barrier();
+        for (int i = threadIdx.x; i < LB * rc; i += kThreads) {
+          const int lb = i / rc, rr = i - lb * rc;
+          cell(ys + lb * 4 * RP, lb, rr);
+        }
+        lds_barrier();
+      } else {
+        for (int lb = 0; lb < LB; ++lb) {
+          const int l = lb / B;
+          const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l);
+          if (!local && !publisher) {
+            // P_x of the next timestep travels while the z words are awaited
+            if (!a.px_all && lb == 0 && t + 1 < T) {
+              float* pxn = pxb + ((t + 1) & 1) * B * OM;
+              for (int i = threadIdx.x; i < B * n_owned; i += gthr) {
+                const int b = i / n_owned, io = i - b * n_owned;
+                pxn[b * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + (t + 1) * B + b];
+              }
+            }
+            // every slot of the exchange whose term is in this level (slots of
+            // workgroups that own fewer terms are skipped by the map check)
+            const int nslots = P * OM;
+            const int GKl = G * Kl;
+            gather_level_any(zs, zmap, a.zx + (size_t)lb * P * OM, nslots, GKl, G, Kmax, tag, a.err, threadIdx.x, gthr);
+          }
+          lds_barrier();
+          if (stamp && lb == 0) a.stamps[4 + 4 * t] = clock64();
+          const float* zl = zs + (local ? lb * GK : 0);
+          if constexpr (UPT > 0) {
+            // branch-free: entries past the budget multiply a valid z by 0
+#pragma unroll
+            for (int o = 0; o < OPT; ++o) {
+              // all z reads first (independent LDS loads in flight), then the FMAs
+              float zv[UPT];
+#pragma unroll
+              for (int k = 0; k < UPT; ++k) {
+                const int n = slb + S0 * k;
+                zv[k] = zl[zbase[o] + (n < Kl ? n : 0)];
+              }
+              float acc = 0.0f;
+#pragma unroll
+              for (int k = 0; k < UPT; ++k) {
+                const int n = slb + S0 * k;
+                acc += (n < Kl ? uv[o * UPT + k] : 0.0f) * zv[k];
+              }
+              acc = group_sum_rt(acc, S0);
+              if (yslot[o] >= 0 && slb == 0) ys[yslot[o]] = acc + bs[yslot[o]];
+            }
+          } else {
+            // S is a power of two (1 .. 16)
+            const int S = __builtin_amdgcn_readlane(vlanes, l), lgS = 31 - __builtin_clz(S);
+            const int OPP = kThreads >> lgS, os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
+            for (int base = 0; base < outs; base += OPP) {
+              const int ol = base + os;
+              float acc = 0.0f;
+              int q = 0, rr = 0;
+              if (ol < outs) {
+                q = ol / rc;
+                rr = ol - q * rc;
+                const float* zg = zl + ((G == 4) ? q : 0) * Kmax;
+                if (a.ustride) {
+                  const float* urow = us + (size_t)(q * RP + rr) * a.ustride;
+#pragma unroll 8
+                  for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+                } else {
+                  const float* urow = a.Ut + (size_t)(q * H + r0 + rr) * N;
+#pragma unroll 8
+                  for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+                }
+              }
+              acc = group_sum_rt(acc, S);
+              if (sl == 0 && ol < outs) ys[q * RP + rr] = acc + bs[q * RP + rr];
+            }
+          }
+          lds_barrier();
+          for (int rr = threadIdx.x; rr < rc; rr += kThreads) {
+            const float gi = sigmoid_fast(ys[0 * RP + rr]);
+            const float gf = sigmoid_fast(ys[1 * RP + rr]);
+            const float gg = tanh_fast(ys[2 * RP + rr]);
+            const float go = sigmoid_fast(ys[3 * RP + rr]);
+            const float c = gf * cs[lb * RP + rr] + gi * gg;
+            const float hv2 = go * tanh_fast(c);
+            cs[lb * RP + rr] = c;
+            hown[lb * RP + rr] = hv2;
+            if (local) hs[lb * H + r0 + rr] = hv2;
+          }
+          lds_barrier();
+        }
       }
     }
     if (stamp) a.stamps[5 + 4 * t] = clock64();
@@ -729,6 +899,10 @@ size_t plan_progressive(RunArgs& a, int P) {
   a.vh_lds = 0;
   a.ustride = 0;
   a.px_all = 0;
+  // several (level, sequence) pairs: one phase-B pass for all of them when
+  // their z fit in LDS next to everything else
+  a.allpairs = (a.L * a.B > 1 && a.GK > 0) ? 1 : 0;
+  if (a.allpairs && layout_of(a, a.online).total > kLdsCap) a.allpairs = 0;
   size_t need = layout_of(a, a.online).total;
   if (need > kLdsCap) return need;
   if (a.hpl == 0) {
@@ -745,10 +919,10 @@ size_t plan_progressive(RunArgs& a, int P) {
   return layout_of(a, a.online).total;
 }
 
-template <int HPL, int OPT, int UPT, bool ONLINE = false>
-hipError_t launch_one(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
+template <int HPL, int OPT, int UPT, bool ONLINE, bool AP>
+hipError_t launch_kernel(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
   static bool attr_set = false;
-  const void* fn = (const void*)progressive_lstm_kernel<HPL, OPT, UPT, ONLINE>;
+  const void* fn = (const void*)progressive_lstm_kernel<HPL, OPT, UPT, ONLINE, AP>;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsCap);
     if (e != hipSuccess) return e;
@@ -759,8 +933,16 @@ hipError_t launch_one(const RunArgs& a, int blocks, int cooperative, size_t lds,
     void* args[] = {&copy};
     return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(kThreads), args, (unsigned)lds, stream);
   }
-  progressive_lstm_kernel<HPL, OPT, UPT, ONLINE><<<dim3(blocks), dim3(kThreads), lds, stream>>>(a);
+  progressive_lstm_kernel<HPL, OPT, UPT, ONLINE, AP><<<dim3(blocks), dim3(kThreads), lds, stream>>>(a);
   return hipGetLastError();
+}
+
+// The all-pairs phase B is compiled only into the instances that launches
+// with several (level, sequence) pairs use: it costs the others registers.
+template <int HPL, int OPT, int UPT, bool ONLINE = false>
+hipError_t launch_one(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
+  if (a.allpairs) return launch_kernel<HPL, OPT, UPT, ONLINE, true>(a, blocks, cooperative, lds, stream);
+  return launch_kernel<HPL, OPT, UPT, ONLINE, false>(a, blocks, cooperative, lds, stream);
 }
 
 template <int HPL>

@@ -64,6 +64,8 @@ struct RunArgs {
   int px_all;      // 1: x-part projections of every timestep resident in LDS
   int xvec;        // 1: x rows may be read as 16-byte vectors (D % 4 == 0, x 16-byte aligned)
   int bulk_h;      // 1: h exchanged in bulk (hbx + hflag), 0: as tagged words (hx)
+  int allpairs;    // 1: phase B takes every (level, sequence) pair in one pass (z of all
+                   //    pairs resident in LDS); 0: one pass per pair
   int hb_stride;   // floats per parity of hbx: L*B*H rounded up to 4
   int P;           // workgroups of the launch
   int lanes_a;     // lanes per term in phase A (16)
