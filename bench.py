@@ -61,9 +61,10 @@ def main():
     ap.add_argument("--time-prepare", default="",
                     help="NAME:RANK:PRUNE -- only time the device factorisation of a named workload "
                          "(e.g. deadline:2048:0.9) and print one JSON line")
-    ap.add_argument("--workload", default="driving", choices=["driving", "batched", "deadline"],
+    ap.add_argument("--workload", default="driving", choices=["driving", "batched", "deadline", "stack"],
                     help="driving: batch 1, fp32 (default line); batched: 256 sequences, bf16 MFMA path; "
-                         "deadline: D=H=2048, T=64, 8 sequences, rank 2048, both deadline modes")
+                         "deadline: D=H=2048, T=64, 8 sequences, rank 2048, both deadline modes; "
+                         "stack: two layers D=4096 -> 1024 -> 1024, T=32, rank 1024, per-layer budgets")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -87,6 +88,9 @@ def main():
         return
     if args.workload == "deadline":
         bench_deadline(args, torch)
+        return
+    if args.workload == "stack":
+        bench_stack(args, torch)
         return
     dev = torch.device("cuda")
     wl = synth.named("driving")
@@ -343,6 +347,92 @@ def anytime_comparison(torch, B, stream):
                                   [(128, 4160), (128, 130), (128, 32), (64, 4160, "non-residual"),
                                    (64, 130, "non-residual")], Kp, rows_p)
     return out
+
+
+def bench_stack(args, torch):
+    """The stacked workload: layer 1 D=4096 -> H=1024, layer 2 1024 -> 1024,
+    T=32, one sequence, fp32, per-layer rank 1024, 75% pruning (NZ = 1280 and
+    512), factorised on the device.  A step is one approx_lstm_run_stack at one
+    pair of per-layer budgets; each layer is one input projection and one
+    persistent recurrence.  The roofline counts both layers' algorithmic
+    bytes (every term streamed once per timestep, the paper's accounting)."""
+    from paper_1905_00689_amd import synth
+    from paper_1905_00689_amd import binding as B
+    dev = torch.device("cuda")
+    wl = synth.named("stack")
+    (W1, b1), (W2, b2) = wl.layers
+    D, H, T, Bn = wl.D, wl.H, wl.T, wl.B
+    rank = 1024
+    t0 = time.time()
+    m1 = B.approx_lstm_prepare(W1[:, :D], W1[:, D:], b1, D, H, rank, prune_ratio=0.75, groups=4,
+                               flags=B.FLAG_DEVICE_FACTORISE)
+    m2 = B.approx_lstm_prepare(W2[:, :H], W2[:, H:], b2, H, H, rank, prune_ratio=0.75, groups=4,
+                               flags=B.FLAG_DEVICE_FACTORISE)
+    prep_s = time.time() - t0
+    nz1, nz2 = m1.info["nz"], m2.info["nz"]
+    x = torch.from_numpy(wl.x).to(dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, steps, warmup):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps   # ms per step
+
+    h = torch.empty((1, T, Bn, H), device=dev)
+    sweep = {"K": [], "us_per_timestep": [], "timesteps_per_s": [], "hbm_frac": []}
+    ms = bytes_step = None
+    for k1, k2 in ((64, 64), (256, 256), (1024, 1024)):
+        ms = timed(lambda: B.approx_lstm_run_stack([m1, m2], x, [(k1, k2)], h, stream=stream),
+                   args.sweep_steps, 5)
+        B.approx_lstm_check(m1)
+        B.approx_lstm_check(m2)
+        bytes_step = T * (algorithmic_bytes_per_timestep(4, H, nz1, D + H, k1, D, H, Bn, 1)
+                          + algorithmic_bytes_per_timestep(4, H, nz2, 2 * H, k2, H, H, Bn, 1))
+        sweep["K"].append([k1, k2])
+        sweep["us_per_timestep"].append(round(ms * 1e3 / T, 4))
+        sweep["timesteps_per_s"].append(round(T * Bn / (ms * 1e-3), 1))
+        sweep["hbm_frac"].append(round(bytes_step / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+    achieved = bytes_step / (ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "one step at budgets (1024, 1024): per layer input_proj_kernel + progressive_lstm_kernel",
+                "bytes_per_launch": bytes_step}
+    # the exact (dense) two-layer LSTM on the same input, layer after layer
+    e1 = B.approx_lstm_exact_prepare(W1[:, :D], W1[:, D:], b1, D, H)
+    e2 = B.approx_lstm_exact_prepare(W2[:, :H], W2[:, H:], b2, H, H)
+    h1 = torch.empty((T, Bn, H), device=dev)
+    h2 = torch.empty((T, Bn, H), device=dev)
+
+    def exact_step():
+        B.approx_lstm_exact_run(e1, x, h1, stream=stream)
+        B.approx_lstm_exact_run(e2, h1, h2, stream=stream)
+
+    ms_exact = timed(exact_step, args.sweep_steps, 5)
+    B.approx_lstm_exact_check(e1)
+    B.approx_lstm_exact_check(e2)
+    out = {
+        "metric": "LSTM timesteps/sec at refinement budget K (and us/timestep vs K)",
+        "value": round(T * Bn / (ms * 1e-3), 1), "unit": "timesteps/s", "n_gpus": 1, "steps": args.sweep_steps,
+        "warmup": 5, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "stacked LSTM D=4096 -> H=1024 -> H=1024, T=32, B=1, per-layer rank 1024, "
+                               f"75% pruning (NZ={nz1}, {nz2}), budgets (1024, 1024)",
+                   "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": [nz1, nz2], "K": [1024, 1024],
+                   "groups": 4, "layers": 2},
+        "us_per_timestep": round(ms * 1e3 / T, 4), "prepare_device_s": round(prep_s, 2), "sweep": sweep,
+        "exact_baseline": {"us_per_timestep": round(ms_exact * 1e3 / T, 4),
+                           "timesteps_per_s": round(T * Bn / (ms_exact * 1e-3), 1)},
+        "roofline": roofline, "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
 
 
 def bench_deadline(args, torch):
