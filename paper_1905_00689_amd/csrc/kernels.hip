@@ -427,9 +427,10 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     }
 
     // ---- phase B: y = b + sum_n z_n u_n for the owned rows, gates, c and h ----
-    if (!ONLINE && GK == 0 && rc > 0) {
-      // every level at K = 0: y is the bias alone (the same values as 0 + b
-      // below), so all (level, sequence) pairs take one pass and one barrier
+    if ((ONLINE ? kcur == 0 : GK == 0) && rc > 0) {
+      // every level at K = 0 (an online run: this timestep's K_t = 0): y is
+      // the bias alone (the same values as 0 + b below), so all (level,
+      // sequence) pairs take one pass and one barrier
       if (stamp) a.stamps[4 + 4 * t] = clock64();
       for (int i = threadIdx.x; i < LB * rc; i += kThreads) {
         const int lb = i / rc, rr = i - lb * rc;
