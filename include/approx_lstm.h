@@ -210,6 +210,50 @@ approx_lstm_status approx_lstm_run_anytime(approx_lstm_model* m, const float* x,
                                            float* h_out, int32_t* k_achieved, float* step_us, void* hip_stream);
 
 /*
+ * approx_lstm_run_schedule -- progressive LSTM with a caller-given budget K_t
+ * for every timestep (Sec. VI-B: the computation of each prediction cut to the
+ * budget available for it).  Runs the same online launch as
+ * approx_lstm_run_anytime (sized for the largest K_t), with K_t taken from
+ * k_sched instead of the device clock: the result is the recurrence of Eq. (1)
+ * with K_t terms per gate at timestep t, then the Sec. II cell update.
+ *
+ *   x, T, B, h0, c0  as for approx_lstm_run (1 <= T <= 65534)
+ *   k_sched          host [T]: K_t, each in [0, rank]
+ *   h_out            device [T][B][H]
+ *   c_out            device [B][H] or NULL: c after the last timestep
+ *
+ * fp32 models only (UNSUPPORTED for factor_dtype 1).  Blocking: synchronises
+ * hip_stream and copies k_sched to the device before the launch, which then
+ * runs asynchronously.  Errors: INVALID_ARG for a null pointer, T or B below
+ * 1, or a K_t outside [0, rank].
+ */
+approx_lstm_status approx_lstm_run_schedule(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                            const float* h0, const float* c0, const int32_t* k_sched,
+                                            float* h_out, float* c_out, void* hip_stream);
+
+/*
+ * approx_lstm_plan -- the launch plan an fp32 run would use, without any
+ * device work (for tests and tuning; no part of the paper's method).
+ *
+ *   T, B               sequence length and count (>= 1)
+ *   levels, n_levels   host [n_levels] budgets as for approx_lstm_run
+ *                      (ignored when online != 0: the plan of an anytime or
+ *                      scheduled run sized for the whole rank)
+ *   num_cu             compute units to plan for (0 = the model's device)
+ *   out                host [8]: workgroups, all-timestep P_x resident in LDS
+ *                      (1/0), all (level, sequence) pairs in one phase-B pass
+ *                      (1/0), h-part entries per lane in registers, U entries
+ *                      per thread in registers, output rows per thread, bulk
+ *                      h exchange (1/0), LDS bytes per workgroup (above
+ *                      163840: the run returns UNSUPPORTED)
+ *
+ * Works on HOST_ONLY models.  Errors: INVALID_ARG for bad sizes or levels;
+ * UNSUPPORTED for bf16 models.
+ */
+approx_lstm_status approx_lstm_plan(const approx_lstm_model* m, int32_t T, int32_t B, const int32_t* levels,
+                                    int32_t n_levels, int32_t online, int32_t num_cu, int32_t* out);
+
+/*
  * approx_lstm_run_stack -- stacked LSTM layers, each progressive: layer l
  * (l >= 1) takes as its input sequence the h_t of layer l-1 at the same level.
  *

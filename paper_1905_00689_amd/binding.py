@@ -63,6 +63,8 @@ _sigs = {
     "approx_lstm_run_stack": [_vp, _i32, _vp, _i32, _i32, _vp, _i32, _vp, _vp],
     "approx_lstm_run_deadline": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
     "approx_lstm_run_anytime": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
+    "approx_lstm_run_schedule": [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp],
+    "approx_lstm_plan": [_vp, _i32, _i32, _vp, _i32, _i32, _i32, _vp],
     "approx_lstm_check": [_vp, _vp],
     "approx_lstm_set_launch": [_vp, _i32, _i32],
     "approx_lstm_set_batched_path": [_vp, _i32],
@@ -192,6 +194,32 @@ def approx_lstm_run_anytime(model, x, deadline_us, h_out, h0=None, c0=None, stre
                                      us.ctypes.data, ctypes.c_void_p(_stream(stream)))
     _check(st)
     return k, us
+
+def approx_lstm_run_schedule(model, x, k_sched, h_out, h0=None, c0=None, c_out=None, stream=None):
+    """Budget K_t given per timestep (host ints, length T).  x [T, B, D],
+    h_out [T, B, H], c_out [B, H] or None, GPU float32."""
+    T, B, D = x.shape
+    H = model.hidden_size
+    ks, kp = _host(k_sched, np.int32)
+    if ks.shape != (T,):
+        raise ValueError(f"k_sched has shape {ks.shape}, expected ({T},)")
+    st = lib.approx_lstm_run_schedule(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)),
+                                      _dev(c0, "c0", (B, H)), kp, _dev(h_out, "h_out", (T, B, H)),
+                                      _dev(c_out, "c_out", (B, H)), ctypes.c_void_p(_stream(stream)))
+    return _check(st)
+
+
+PLAN_FIELDS = ("blocks", "px_all", "allpairs", "hpl", "upt", "opt", "bulk_h", "lds_bytes")
+
+
+def approx_lstm_plan(model, T, B, levels=None, online=0, num_cu=0):
+    """Launch plan of an fp32 run (no device work): dict of PLAN_FIELDS."""
+    lv = levels if levels is not None else [0]
+    arr, ap = _host(lv, np.int32)
+    out = np.zeros(8, np.int32)
+    _check(lib.approx_lstm_plan(model.handle, T, B, ap, len(arr), int(online), int(num_cu), out.ctypes.data))
+    return dict(zip(PLAN_FIELDS, (int(v) for v in out)))
+
 
 def approx_lstm_run_stack(models, x, levels, h_out, stream=None):
     """models: list of Model; x [T, B, D0]; levels: [n_levels][n_layers] ints;

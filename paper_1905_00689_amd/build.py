@@ -9,6 +9,7 @@ written next to this file, where ``binding`` loads it.
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -36,16 +37,23 @@ def _run(cmd, verbose):
     return r
 
 
+HIP_SOURCES = ("kernels.hip", "batched.hip", "exact.hip", "factorise_device.hip", "api.hip")
+
+
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
-    objs = []
     fo = os.path.join(BUILD, "factorise.o")
-    _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, "factorise.cpp"), "-o", fo], verbose)
-    objs.append(fo)
-    for src in ("kernels.hip", "batched.hip", "exact.hip", "factorise_device.hip", "api.hip"):
+    steps = [["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, "factorise.cpp"), "-o", fo]]
+    objs = [fo]
+    for src in HIP_SOURCES:
         o = os.path.join(BUILD, src.replace(".hip", ".o"))
-        _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", o], verbose)
+        steps.append([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", o])
         objs.append(o)
+    # the objects are independent: compile them side by side
+    workers = max(1, min(len(steps), os.cpu_count() or 1, 8))
+    with ThreadPoolExecutor(max_workers=workers) as pool:
+        for f in [pool.submit(_run, cmd, verbose) for cmd in steps]:
+            f.result()
     tmp = OUT + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs, "-lgomp", "-lpthread"], verbose)
     os.replace(tmp, OUT)

@@ -371,8 +371,8 @@ approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int 
 
 // Workgroups for a run: about one per 32 terms in use (so that every
 // workgroup's terms and rows fit registers), at most 256.
-int auto_blocks(const approx_lstm_model* m, int GK, int LB, int LB_seq) {
-  int cap = std::max(1, std::min(m->num_cu, 256));
+int auto_blocks(const approx_lstm_model* m, int GK, int LB, int LB_seq, int num_cu) {
+  int cap = std::max(1, std::min(num_cu, 256));
   // without terms the workgroups are independent (no exchange): spread the
   // cell updates, about 256 (unit, sequence) pairs per workgroup
   // with several sequences every workgroup's rows serve each of them: widen
@@ -401,19 +401,20 @@ struct OnlineCfg {
   int k[alstm::kMaxOptions];
   unsigned ticks[alstm::kMaxOptions];
   unsigned long long budget = 0;
+  const int* sched = nullptr;   // device [T]: K_t given by the caller instead of the clock
 };
 
-// The fp32 progressive run (argument checks done by the caller): fixed
-// levels, or with `on` one online level sized for the whole rank.
-approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t T, int32_t B, const float* h0,
-                                   const float* c0, const int32_t* levels, int32_t n_levels, int kmax, float* h_out,
-                                   float* c_out, hipStream_t stream, const OnlineCfg* on) {
-  alstm::RunArgs a{};
+// Launch plan of an fp32 progressive run: fills the shape fields of `a` and
+// the workgroup count; returns the LDS bytes per workgroup (> kLdsCap: the
+// run does not fit).  num_cu: compute units of the device.
+size_t plan_run(const approx_lstm_model* m, alstm::RunArgs& a, int32_t T, int32_t B, const int32_t* levels,
+                int32_t n_levels, int kmax, const OnlineCfg* on, int num_cu, int* blocks) {
+  a = alstm::RunArgs{};
   a.D = m->D; a.H = m->H; a.G = m->G; a.N = m->N; a.NZ = m->NZ; a.T = T; a.B = B; a.L = n_levels;
   a.GK = m->G * kmax;
   for (int l = 0; l < n_levels; ++l) a.levels[l] = levels[l];
   if (on) {
-    // one level sized for the full rank; the kernel picks K_t per timestep
+    // one level sized for the largest budget; the kernel takes K_t per timestep
     a.online = 1;
     a.n_opts = on->n;
     for (int i = 0; i < on->n; ++i) {
@@ -421,30 +422,44 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
       a.opt_ticks[i] = on->ticks[i];
     }
     a.budget = on->budget;
+    a.sched = on->sched;
   }
   a.hcap = a.GK > 0 ? m->hpre[a.GK - 1] : 0;
   a.lanes_a = alstm::lanes_for_terms(m->NZ, m->D, m->H);
   for (int l = 0; l < n_levels; ++l) a.lanes_b[l] = alstm::lanes_for_level(levels[l]);
-  const int maxP = std::max(1, m->num_cu);
-  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK, n_levels * B, B);
+  const int maxP = std::max(1, num_cu);
+  int P = m->launch_blocks > 0 ? std::min(m->launch_blocks, maxP) : auto_blocks(m, a.GK, n_levels * B, B, num_cu);
   size_t lds = alstm::plan_progressive(a, P);
   if (m->launch_blocks == 0)   // automatic: widen until the per-workgroup slices fit in LDS
     while (lds > alstm::kLdsCap && P < maxP) {
       P = std::min(maxP, 2 * P);
       lds = alstm::plan_progressive(a, P);
     }
+  *blocks = P;
+  return lds;
+}
+
+// The fp32 progressive run (argument checks done by the caller): fixed
+// levels, or with `on` one online level sized for kmax.
+approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t T, int32_t B, const float* h0,
+                                   const float* c0, const int32_t* levels, int32_t n_levels, int kmax, float* h_out,
+                                   float* c_out, hipStream_t stream, const OnlineCfg* on) {
+  alstm::RunArgs a{};
+  int P = 1;
+  const size_t lds = plan_run(m, a, T, B, levels, n_levels, kmax, on, m->num_cu, &P);
   const size_t LB = (size_t)n_levels * B;
   if (lds > alstm::kLdsCap)
     return fail(APPROX_LSTM_ERR_UNSUPPORTED, "LDS need %zu bytes exceeds 160 KiB (H=%d, levels*B=%zu, G*K=%d)",
                 lds, m->H, LB, a.GK);
 
   const size_t kword = on ? 1 : 0;   // K_t of an online run rides with h
+  // h words per step parity (tagged words in hx, floats in the bulk hbx)
+  a.hb_stride = (int)round_up(LB * m->H + kword, 4);
   approx_lstm_status st =
       ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * P * a.owned_max),
-                       LB * m->H + kword, stream);
+                       2 * (size_t)a.hb_stride, stream);
   if (st != APPROX_LSTM_OK) return st;
   a.bulk_h = alstm::use_bulk_h(n_levels, B, m->H);
-  a.hb_stride = (int)round_up(LB * m->H + kword, 4);
   if (a.bulk_h) {
     st = ensure_bulk(m, 2 * (size_t)a.hb_stride, stream);
     if (st != APPROX_LSTM_OK) return st;
@@ -603,6 +618,18 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
     return fail(APPROX_LSTM_ERR_DEVICE, "factorisation failed: %s", ex.what());
   }
 
+  {
+    // h-part entry counts (entries of prune(v) at columns >= D), running
+    // maximum over the terms in refinement order: sizes the launch plan
+    const size_t NT = (size_t)N * G;
+    m->hpre.resize(NT);
+    for (size_t tau = 0; tau < NT; ++tau) {
+      const size_t src = (tau % G) * N + tau / G;
+      int h = 0;
+      for (int e = 0; e < nz; ++e) h += m->vidx[src * nz + e] >= D ? 1 : 0;
+      m->hpre[tau] = tau ? std::max(m->hpre[tau - 1], h) : h;
+    }
+  }
   if (!host_only) {
     // Pack the device store: term tau = n*G + g in refinement order.
     const size_t NT = (size_t)N * G;
@@ -621,11 +648,6 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
         }
         nx_h[tau] = (uint16_t)cnt;
       }
-    m->hpre.resize(NT);
-    for (size_t tau = 0; tau < NT; ++tau) {
-      const int h = nz - nx_h[tau];
-      m->hpre[tau] = tau ? std::max(m->hpre[tau - 1], h) : h;
-    }
     for (int o = 0; o < 4 * H; ++o) {
       const int g = o / Rg, r = o % Rg;
       for (int n = 0; n < N; ++n) Ut_h[(size_t)o * N + n] = m->u[((size_t)g * N + n) * Rg + r];
@@ -710,9 +732,11 @@ approx_lstm_status approx_lstm_reserve(approx_lstm_model* m, int32_t T_max, int3
   }
   const size_t GK = (size_t)m->G * m->N, LB = (size_t)L_max * B_max;
   const size_t P_max = std::max(1, m->num_cu);
-  st = ensure_workspace(m, GK * T_max * B_max, LB * (GK + P_max), LB * m->H, nullptr);
+  // h exchange: two step-parity halves of L*B*H words plus an online run's K word
+  const size_t hhalf = round_up(LB * m->H + 1, 4);
+  st = ensure_workspace(m, GK * T_max * B_max, LB * (GK + P_max), 2 * hhalf, nullptr);
   if (st == APPROX_LSTM_OK && alstm::use_bulk_h(L_max, B_max, m->H))
-    st = ensure_bulk(m, 2 * round_up(LB * m->H, 4), nullptr);
+    st = ensure_bulk(m, 2 * hhalf, nullptr);
   if (st != APPROX_LSTM_OK) return st;
   HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
   return APPROX_LSTM_OK;
@@ -1025,6 +1049,80 @@ approx_lstm_status approx_lstm_run_anytime(approx_lstm_model* m, const float* x,
   HIP_TRY(hipMemcpy(k_achieved, m->d_kt, (size_t)T * sizeof(int32_t), hipMemcpyDeviceToHost), "read budgets");
   if (step_us)
     for (int t = 0; t < T; ++t) step_us[t] = (float)steps[t];
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status approx_lstm_run_schedule(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                            const float* h0, const float* c0, const int32_t* k_sched, float* h_out,
+                                            float* c_out, void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (!m->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "model has no device store (HOST_ONLY)");
+  if (T < 1 || B < 1 || !x || !h_out || !k_sched) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
+  if (T > 65534) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T = %d exceeds 65534", T);
+  if (m->dtype != 0) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "scheduled runs need an fp32 model");
+  int kmax = 0;
+  for (int t = 0; t < T; ++t) {
+    if (k_sched[t] < 0 || k_sched[t] > m->N)
+      return fail(APPROX_LSTM_ERR_INVALID_ARG, "timestep %d: K = %d not in [0, %d]", t, k_sched[t], m->N);
+    kmax = std::max(kmax, (int)k_sched[t]);
+  }
+  DeviceScope ds(m->device);
+  if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  hipStream_t stream = (hipStream_t)hip_stream;
+  // the schedule goes to the model's budget array (no run may still read it)
+  HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+  if ((size_t)T > m->kt_cap) {
+    dfree(m->d_kt);
+    m->kt_cap = 0;
+    HIP_TRY(hipMalloc(&m->d_kt, (size_t)T * sizeof(int)), "hipMalloc(kt)");
+    m->kt_cap = T;
+  }
+  HIP_TRY(hipMemcpy(m->d_kt, k_sched, (size_t)T * sizeof(int32_t), hipMemcpyHostToDevice), "copy schedule");
+  OnlineCfg cfg;
+  cfg.n = 1;
+  cfg.k[0] = kmax;
+  cfg.ticks[0] = 0;
+  cfg.budget = 1ull << 40;
+  cfg.sched = m->d_kt;
+  return run_progressive(m, x, T, B, h0, c0, &kmax, 1, kmax, h_out, c_out, stream, &cfg);
+}
+
+approx_lstm_status approx_lstm_plan(const approx_lstm_model* m, int32_t T, int32_t B, const int32_t* levels,
+                                    int32_t n_levels, int32_t online, int32_t num_cu, int32_t* out) {
+  g_last_error.clear();
+  if (!m || !out || T < 1 || B < 1 || num_cu < 0) return fail(APPROX_LSTM_ERR_INVALID_ARG, "bad arguments");
+  if (m->dtype != 0) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "launch plans describe fp32 models");
+  int kmax = 0;
+  std::vector<int32_t> lv;
+  if (online) {
+    kmax = m->N;
+    lv.push_back(kmax);
+  } else {
+    if (!levels || n_levels < 1 || n_levels > APPROX_LSTM_MAX_LEVELS)
+      return fail(APPROX_LSTM_ERR_INVALID_ARG, "need 1..%d levels", APPROX_LSTM_MAX_LEVELS);
+    for (int l = 0; l < n_levels; ++l) {
+      if (levels[l] < 0 || levels[l] > m->N)
+        return fail(APPROX_LSTM_ERR_INVALID_ARG, "level %d: K = %d not in [0, %d]", l, levels[l], m->N);
+      kmax = std::max(kmax, (int)levels[l]);
+      lv.push_back(levels[l]);
+    }
+  }
+  OnlineCfg cfg;
+  cfg.n = 1;
+  cfg.k[0] = kmax;
+  alstm::RunArgs a{};
+  int P = 1;
+  const size_t lds = plan_run(m, a, T, B, lv.data(), (int)lv.size(), kmax, online ? &cfg : nullptr,
+                              num_cu > 0 ? num_cu : m->num_cu, &P);
+  out[0] = P;
+  out[1] = a.px_all;
+  out[2] = a.allpairs;
+  out[3] = a.hpl;
+  out[4] = a.upt;
+  out[5] = a.opt;
+  out[6] = alstm::use_bulk_h((int)lv.size(), B, m->H);
+  out[7] = (int32_t)std::min<size_t>(lds, 0x7fffffff);
   return APPROX_LSTM_OK;
 }
 

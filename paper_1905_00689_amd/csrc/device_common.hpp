@@ -130,12 +130,18 @@ __device__ __forceinline__ void store_coherent(float* p, float v) {
   __hip_atomic_store(reinterpret_cast<unsigned*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// threads tid < nthr poll flags [0, P) until each holds `tag` (bounded)
+// 1 when flag word w carries `tag` or a later timestep's tag of the same
+// launch (tag = launch sequence << 16 | timestep + 1)
+__device__ __forceinline__ bool flag_reached(unsigned w, unsigned tag) {
+  return (w >> 16) == (tag >> 16) && (w & 0xFFFFu) >= (tag & 0xFFFFu);
+}
+
+// threads tid < nthr poll flags [0, P) until each has reached `tag` (bounded)
 __device__ __forceinline__ void await_flags(const unsigned* flag, int P, unsigned tag, unsigned* err, int tid,
                                             int nthr) {
   for (int f = tid; f < P; f += nthr) {
     unsigned spins = 0;
-    while (__hip_atomic_load(flag + f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != tag) {
+    while (!flag_reached(__hip_atomic_load(flag + f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), tag)) {
       __builtin_amdgcn_s_sleep(2);
       if ((++spins & 255u) == 0u &&
           (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {

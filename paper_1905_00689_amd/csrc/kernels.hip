@@ -1,18 +1,22 @@
 // gfx950 kernels for progressive approximate-LSTM inference
 // (arXiv 1905.00689, Sec. III Eq. (1) per gate, then the Sec. II cell update).
 //
-// One persistent launch runs a whole sequence.  Workgroup j of P owns the
-// refinement terms tau = j, j+P, j+2P, ... (round-robin, so every prefix K is
-// spread over all workgroups) and a contiguous slice of hidden units (all
-// four gates of each).  The prologue computes the x-part projections of the
-// owned terms for every timestep (they do not depend on h) and copies the
-// owned terms' h-part entries, sigma and the owned rows of U into LDS, where
-// they stay for the whole sequence.  Per timestep:
+// input_proj_kernel computes, before the recurrence and over the whole GPU,
+// the x-part projections P_x = prune(v)_x . x_t of every term in use and
+// every timestep (they do not depend on h).  Then one persistent launch runs
+// the whole sequence.  Workgroup j of P owns the refinement terms tau = j,
+// j+P, j+2P, ... (round-robin, so every prefix K is spread over all
+// workgroups) and a contiguous slice of hidden units (all four gates of
+// each).  The prologue loads the owned terms' h-part entries and the owned
+// rows of U into registers (HPL / UPT instances; LDS, or for U global memory,
+// where they do not fit) and sigma, the bias and P_x into LDS, where they
+// stay for the whole sequence.  Per timestep:
 //   phase A  for each owned term: s = P_x + prune(v)_h . h_{t-1};  z = sigma*s;
 //            z is published as a tagged 64-bit word;
 //   phase B  gather every z of the level, accumulate y = b + sum_n z_n u_n for
 //            the owned rows of all four gates, apply the gate nonlinearities
-//            and the c/h update, publish h as tagged words;
+//            and the c/h update, publish h (tagged words, or in bulk behind
+//            one flag word per workgroup);
 //   phase C  gather the full h_t for the next timestep.
 // The exchanges use relaxed agent-scope 64-bit atomics whose upper half is a
 // per-launch, per-timestep tag: a reader spins until the tag it expects
@@ -362,10 +366,10 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
   unsigned long long t_begin = 0ull;
   int kcur = 0;
   if constexpr (ONLINE) {
-    kcur = online_pick(a, (long long)a.budget);
+    kcur = a.sched ? a.sched[0] : online_pick(a, (long long)a.budget);
     if (chooser) {
       t_begin = wall_clock64();
-      a.kt[0] = kcur;
+      if (!a.sched) a.kt[0] = kcur;
     }
   }
   for (int t = 0; t < T; ++t) {
@@ -417,6 +421,17 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     }
     lds_barrier();
     if (stamp) a.stamps[3 + 4 * t] = clock64();
+    // P_x of the next timestep (when not all resident) travels while this
+    // timestep's z are exchanged.  Its slot (t+1)&1 was last read by phase A
+    // of timestep t-1; every branch below (K_t = 0 included) and a single
+    // workgroup take it here, so timestep t+1 never reads a stale slot.
+    if (!a.px_all && t + 1 < T && !publisher) {
+      float* pxn = pxb + ((t + 1) & 1) * B * OM;
+      for (int i = threadIdx.x; i < B * n_owned; i += gthr) {
+        const int b = i / n_owned, io = i - b * n_owned;
+        pxn[b * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + (t + 1) * B + b];
+      }
+    }
     if (publisher && !local) {
       for (int lb = 0; lb < LB; ++lb) {
         const int GKl = G * (ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, lb / B));
@@ -449,16 +464,6 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
       if constexpr (AP) {
         // every pair at once: one gather of all their z, one accumulation
         // pass, one cell-update pass.
-        // The x-part projections of the next timestep travel while z is awaited.
-        auto prefetch_px = [&]() {
-          if (!a.px_all && t + 1 < T) {
-            float* pxn = pxb + ((t + 1) & 1) * B * OM;
-            for (int i = threadIdx.x; i < B * n_owned; i += gthr) {
-              const int b = i / n_owned, io = i - b * n_owned;
-              pxn[b * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + (t + 1) * B + b];
-            }
-          }
-        };
         // y of the owned rows of one pair: yl[q*RP + rr] = b + sum_{n<Kl} u z
         auto accumulate = [&](const float* zl, float* yl, int Kl, int l) {
           if constexpr (UPT > 0) {
@@ -521,7 +526,6 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           if (local) hs[lb * H + r0 + rr] = hv2;
         };
         if (!local && !publisher) {
-          prefetch_px();
           const int nslots = P * OM, n = LB * nslots, per = (n + gthr - 1) / gthr;
           const int kc = ONLINE ? kcur : -1;
           if (per <= 1)
@@ -550,14 +554,6 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           const int l = lb / B;
           const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l);
           if (!local && !publisher) {
-            // P_x of the next timestep travels while the z words are awaited
-            if (!a.px_all && lb == 0 && t + 1 < T) {
-              float* pxn = pxb + ((t + 1) & 1) * B * OM;
-              for (int i = threadIdx.x; i < B * n_owned; i += gthr) {
-                const int b = i / n_owned, io = i - b * n_owned;
-                pxn[b * OM + io] = a.px[(size_t)(j + io * P) * (T * B) + (t + 1) * B + b];
-              }
-            }
             // every slot of the exchange whose term is in this level (slots of
             // workgroups that own fewer terms are skipped by the map check)
             const int nslots = P * OM;
@@ -632,16 +628,19 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     if (stamp) a.stamps[5 + 4 * t] = clock64();
     // without terms (every level K = 0) no workgroup reads another's h
     const bool exch = !local && GK > 0;
+    // h_t (and an online run's K_{t+1}) travel in the half of the exchange
+    // selected by step parity, tagged words and bulk alike
     float* hbt = a.bulk_h ? a.hbx + (size_t)(t & 1) * a.hb_stride : nullptr;
+    unsigned long long* hxt = a.hx + (size_t)(t & 1) * a.hb_stride;
     if (ONLINE && chooser && t + 1 < T) {
       // K_{t+1}: timestep t+1 must end by (t+2) * budget after the start
       const long long used = (long long)(wall_clock64() - t_begin);
-      const int knext = online_pick(a, (long long)(t + 2) * (long long)a.budget - used);
-      a.kt[t + 1] = knext;
+      const int knext = a.sched ? a.sched[t + 1] : online_pick(a, (long long)(t + 2) * (long long)a.budget - used);
+      if (!a.sched) a.kt[t + 1] = knext;
       const float kbits = __int_as_float(knext);
       if (local) hs[LB * H] = kbits;
       else if (a.bulk_h) store_coherent(hbt + (size_t)LB * H, kbits);
-      else publish(a.hx + (size_t)LB * H, kbits, tag);
+      else publish(hxt + (size_t)LB * H, kbits, tag);
     }
     if (publisher) {
       for (int lb = 0; lb < LB; ++lb) {
@@ -652,7 +651,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           a.h_out[(((size_t)l * T + t) * B + b) * H + r] = h2;
           if (exch) {
             if (a.bulk_h) store_coherent(hbt + (size_t)lb * H + r, h2);
-            else publish(a.hx + (size_t)lb * H + r, h2, tag);
+            else publish(hxt + (size_t)lb * H + r, h2, tag);
           }
         }
       }
@@ -666,14 +665,18 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     const int online_word = (ONLINE && t + 1 < T) ? 1 : 0;
     if (exch) {
       if (a.bulk_h) {
-        // h_t is double-buffered by step parity: a workgroup can publish
-        // h_{t+1} only after every z of step t+1, i.e. after every workgroup
-        // has finished reading h_t
+        // h_t is double-buffered by step parity.  A workgroup publishes
+        // h_{t+2} (into this half again) only after it has gathered h_{t+1}
+        // from every workgroup, and each publishes h_{t+1} only after
+        // reading h_t: so no half is overwritten while it is still read,
+        // even at online timesteps with K_t = 0, which exchange no z.  A
+        // flag may then already carry tag t+2 (its owner one step ahead,
+        // writing the other half), which await_flags accepts.
         if (!publisher) await_flags(a.hflag, P, tag, a.err, threadIdx.x, gthr);
         lds_barrier();
         if (!publisher) read_coherent(hs, hbt, LB * H + online_word, threadIdx.x, gthr);
       } else if (!publisher) {
-        gather_tagged<2>(hs, nullptr, a.hx, LB * H + online_word, tag, a.err, threadIdx.x, gthr);
+        gather_tagged<2>(hs, nullptr, hxt, LB * H + online_word, tag, a.err, threadIdx.x, gthr);
       }
     }
     lds_barrier();

@@ -25,7 +25,8 @@ constexpr size_t kLdsCap = 160 * 1024; // LDS per CU on gfx950
 //   px     [GK][T*B]            x-part projections (workspace, written by input_proj_kernel)
 //   zx     [L*B][P][owned_max] u64  tagged z exchange (value | tag << 32), slot
 //                                   j*owned_max + i carries term j + i*P
-//   hx     [L*B][H] u64         tagged h exchange (few values per workgroup)
+//   hx     [2][hb_stride] u64   tagged h exchange (few values per workgroup): h_t of every
+//                                (level, seq) and an online run's K_{t+1} in half t & 1
 //   hbx, hflag                  bulk h exchange (many values: large L*B*H)
 struct RunArgs {
   const float* x;
@@ -66,7 +67,7 @@ struct RunArgs {
   int bulk_h;      // 1: h exchanged in bulk (hbx + hflag), 0: as tagged words (hx)
   int allpairs;    // 1: phase B takes every (level, sequence) pair in one pass (z of all
                    //    pairs resident in LDS); 0: one pass per pair
-  int hb_stride;   // floats per parity of hbx: L*B*H rounded up to 4
+  int hb_stride;   // words per step parity of hx and hbx: L*B*H (+1 online) rounded up to 4
   int P;           // workgroups of the launch
   int lanes_a;     // lanes per term in phase A (16)
   unsigned tag_base;
@@ -84,6 +85,9 @@ struct RunArgs {
   unsigned opt_ticks[kMaxOptions];  // predicted wall ticks of one timestep at that budget
   unsigned long long budget;        // wall ticks per timestep
   int* kt;                          // [T] chosen budgets (written by workgroup 0)
+  const int* sched;                 // null, or device [T]: K_t given by the caller (read by
+                                    // workgroup 0 in place of the clock-based choice; every
+                                    // other step of an online run unchanged)
 };
 
 // Budget of an online run for `avail` wall ticks: the largest option that

@@ -136,6 +136,47 @@ def test_driving_all_budgets_match_oracle_on_exported_terms(driving, driving_p75
         assert rel_err(h[j], ho[j]) < TOL, (K, rel_err(h[j], ho[j]))
 
 
+@pytest.fixture(scope="module", params=[0.5, 0.9], ids=["p50", "p90"])
+def driving_other(request, driving):
+    p = request.param
+    say(f"prepare driving p={p} rank 512")
+    return p, prep(driving, 512, p)
+
+
+def test_driving_other_ratios_early_levels_match_independent_oracle(driving, driving_other):
+    """The driving workload's other pruning ratios (NZ = 1280 at 50%, 256 at
+    90%): budgets inside the chain-agreement horizon (24 steps at 50%, 16 at
+    90%) against factors the oracle prepares itself."""
+    p, m = driving_other
+    nz = oracle.nz_from_ratio(2560, p)
+    levels = [1, 2, 4, 8, 16, 24] if p < 0.9 else [1, 2, 4, 8, 16]
+    say(f"driving p={p} (NZ={nz}) levels", levels, "vs oracle-prepared factors")
+    f = oracle.prepare(driving.W, 512, max(levels), nz)
+    h, _ = run_gpu(m, driving.x, levels)
+    ho, _ = oracle.run(f, driving.b, driving.x, levels)
+    for j, K in enumerate(levels):
+        e = rel_err(h[j], ho[j])
+        say("  K", K, "rel err", e)
+        assert e < TOL, (K, e)
+
+
+def test_driving_other_ratios_all_budgets_on_exported_terms(driving, driving_other):
+    p, m = driving_other
+    levels = [32, 64, 128, 256, 512]
+    say(f"driving p={p} levels", levels, "vs oracle on exported terms")
+    f = exported_factors(m)
+    h, _ = run_gpu(m, driving.x, levels)
+    ho, _ = oracle.run(f, driving.b, driving.x, levels)
+    for j, K in enumerate(levels):
+        e = rel_err(h[j], ho[j])
+        say("  K", K, "rel err", e)
+        assert e < TOL, (K, e)
+    # each budget alone: the bench's single-level launch shape
+    for K in (64, 512):
+        alone, _ = run_gpu(m, driving.x, [K])
+        assert rel_err(alone[0], ho[levels.index(K)]) < TOL, K
+
+
 def test_driving_levels_are_bitwise_independent(driving, driving_p75):
     say("driving level independence")
     together, _ = run_gpu(driving_p75, driving.x, [512, 1, 64])

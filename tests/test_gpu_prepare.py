@@ -165,6 +165,22 @@ def test_deadline_workload_full_rank_on_device():
         e = rel_err(h.cpu().numpy()[0], ho[0])
         say("  K", K, "rel err", e)
         assert e < 1e-4, (K, e)
+    # both deadline modes at 100 us per timestep on the full-rank model (the
+    # anytime launch holds all 2048 terms per gate, its U rows read from
+    # memory), each replayed by the oracle at the budgets it reports
+    hd = torch.full((w.T, w.B, w.H), float("nan"), device="cuda")
+    for mode, fn in (("one K", B.approx_lstm_run_deadline), ("K_t per step", B.approx_lstm_run_anytime)):
+        say("  deadline 100 us,", mode)
+        k, us = fn(m, x, 100.0, hd)
+        B.approx_lstm_check(m)
+        torch.cuda.synchronize()
+        ks = [int(v) for v in k]
+        say("    K_t min/mean/max", min(ks), float(np.mean(ks)), max(ks), "mean step us", float(np.mean(us)))
+        assert all(0 <= v <= 2048 for v in ks)
+        ho, _ = oracle.run_schedule(f, w.b, w.x, ks)
+        e = rel_err(hd.cpu().numpy(), ho)
+        say("    rel err vs oracle replay", e)
+        assert e < 1e-4, (mode, e)
 
 
 @pytest.mark.parametrize("G", [4, 1])

@@ -129,6 +129,77 @@ def test_driving_full_chain_certificates(driving, driving_full_p75):
                 assert abs(np.sum(R * R) - acc) <= 1e-9 * e0, (g, n)
 
 
+def test_driving_full_chain_p13_every_step(driving, driving_full_p75):
+    """P13 certificates at every step of the rank-512 chain at 75% pruning,
+    all four gates: (ii) the exported unpruned v_n and u_n are the top
+    singular pair of the residual the earlier terms leave, ||R v_n - sigma_n
+    u_n|| and ||R^T u_n - sigma_n v_n|| <= 1e-10 sigma_1; (iii) the stored
+    mask equals the NZ largest magnitudes of v_n (lower index first on
+    ties), bit-exactly (Sec. III: prune(v, NZ) of Eq. (1))."""
+    m = driving_full_p75
+    W = driving.W.astype(np.float64)
+    for g in range(4):
+        R = W[g * 512:(g + 1) * 512].copy()
+        lf = B.approx_lstm_get_factors(m, g)
+        l64 = B.approx_lstm_get_factors_f64(m, g)
+        sig, U, V = l64["sigma"], l64["u"], l64["v"]
+        idx = lf["v_idx"].astype(np.int64)
+        s1 = sig[0]
+        worst = 0.0
+        for n in range(512):
+            mask = oracle.magnitude_mask(V[n], 640)
+            assert np.array_equal(mask, idx[n]), (g, n)
+            r1 = np.linalg.norm(R @ V[n] - sig[n] * U[n])
+            r2 = np.linalg.norm(R.T @ U[n] - sig[n] * V[n])
+            worst = max(worst, r1, r2)
+            assert r1 <= 1e-10 * s1 and r2 <= 1e-10 * s1, (g, n, r1, r2)
+            R[:, idx[n]] -= sig[n] * np.outer(U[n], V[n][idx[n]])
+        print(f"gate {g}: worst singular-pair residual {worst / s1:.2e} sigma_1 over 512 steps")
+
+
+def test_launch_plans_of_the_tested_shapes():
+    """approx_lstm_plan (no device work) on host-only models: the shapes the
+    GPU tests use reach the launch paths they are meant to cover, in
+    particular P_x streamed one timestep ahead (px_all 0) on each exchange
+    path and on a single workgroup, and the plan of the timed workload."""
+    tiny = synth.make(64, 32, 600, 1, index=44, xkind="normal")
+    m = prep(tiny, 32, p=0.5, flags=B.FLAG_HOST_ONLY)
+    B.approx_lstm_set_launch(m, 2, 0)
+    p = B.approx_lstm_plan(m, 600, 1, online=1, num_cu=256)
+    assert (p["blocks"], p["px_all"], p["bulk_h"]) == (2, 0, 0), p
+    p = B.approx_lstm_plan(m, 200, 1, online=1, num_cu=256)
+    assert (p["blocks"], p["px_all"]) == (2, 1), p
+    B.approx_lstm_set_launch(m, 1, 0)
+    for online in (0, 1):
+        p = B.approx_lstm_plan(m, 300, 1, [32], online=online, num_cu=256)
+        assert (p["blocks"], p["px_all"]) == (1, 0), p
+        p = B.approx_lstm_plan(m, 8, 1, [32], online=online, num_cu=256)
+        assert (p["blocks"], p["px_all"]) == (1, 1), p
+    B.approx_lstm_set_launch(m, 0, 0)
+    p = B.approx_lstm_plan(m, 8, 1, [0, 1, 4, 16, 32], num_cu=256)
+    assert p["allpairs"] == 1 and p["px_all"] == 1, p
+    wide = synth.make(512, 512, 48, 8, index=43, xkind="relu")
+    m2 = prep(wide, 128, p=0.75, flags=B.FLAG_HOST_ONLY)
+    B.approx_lstm_set_launch(m2, 8, 0)
+    p = B.approx_lstm_plan(m2, 48, 8, online=1, num_cu=256)
+    assert (p["px_all"], p["bulk_h"], p["allpairs"]) == (0, 1, 1), p
+    B.approx_lstm_set_launch(m2, 0, 0)
+    p = B.approx_lstm_plan(m2, 48, 8, online=1, num_cu=256)
+    assert (p["px_all"], p["bulk_h"], p["allpairs"]) == (1, 1, 1), p
+    with pytest.raises(B.ApproxLstmError) as ei:
+        B.approx_lstm_plan(m2, 48, 8, [129], num_cu=256)
+    assert ei.value.status == B.ERR_INVALID_ARG
+
+
+def test_driving_plan_of_the_timed_workload(driving, driving_full_p75):
+    """The timed workload (driving shape, K = 512, one sequence, T = 16) on
+    256 compute units: P_x of every timestep resident, register-resident
+    h-part entries and U rows, tagged h words."""
+    p = B.approx_lstm_plan(driving_full_p75, 16, 1, [512], num_cu=256)
+    assert p["px_all"] == 1 and p["bulk_h"] == 0 and p["hpl"] > 0 and p["upt"] > 0, p
+    assert p["lds_bytes"] <= 160 * 1024, p
+
+
 def test_driving_no_pruning_gives_the_svd(driving):
     """NZ = C: the chain is the SVD of each gate (P4), over all 512 steps."""
     m = prep(driving, 512, p=0.0)

@@ -400,6 +400,43 @@ def test_bf16_operand_error_within_the_rounding_bound():
     assert 0 < diff <= 1.5 * dy.max()
 
 
+def test_bf16_rounds_z_itself_hand_worked():
+    """Where the bf16 configuration rounds (Q14 reading of Eq. (1) with bf16
+    operands): z = sigma * s, then z is rounded before it meets u.  One
+    timestep, H = 1, each gate's 1 x 3 block sigma_g u_g e_0^T (so v = e_0,
+    one kept entry, u = +-1, sigma in {3, 5, 7}: all bf16 values), x_0 =
+    1 + 2^-7 (a bf16 value), h0 = c0 = 0, so s = x_0 and sigma * s is exact in
+    float64 but needs 9 significant bits.  Worked by hand, nearest even at 8
+    bits:
+        3 * (1 + 2^-7) = 11.0000011b -> tie, odd kept bit  -> 11.000010b = 3.03125
+        5 * (1 + 2^-7) = 101.0000101b -> below half        -> 101.00001b = 5.03125
+        7 * (1 + 2^-7) = 111.0000111b -> above half        -> 111.00010b = 7.0625
+    so the gate pre-activations are b_g + u_g * z16_g exactly, and the run
+    must equal the exact LSTM with zero weights and that bias.  Not rounding
+    z, or rounding y = b + z u instead of z, gives different outputs (the
+    biases are chosen so that those roundings disagree)."""
+    x0 = 1.0 + 2.0 ** -7
+    sig = np.array([3.0, 5.0, 3.0, 7.0])
+    u = np.array([1.0, -1.0, 1.0, 1.0])
+    z16 = np.array([3.03125, 5.03125, 3.03125, 7.0625])
+    b = np.array([2.0 ** -8, -0.75, 0.5, 2.0 ** -7])
+    W = np.zeros((4, 3))
+    W[:, 0] = sig * u
+    x = np.array([[[x0, 0.5]]])
+    assert np.array_equal(oracle.round_bf16(sig * x0), z16)
+    f = oracle.prepare(W, 1, 1, 1).rounded("bf16")
+    assert np.array_equal(f.sigma[:, 0], sig) and np.all(f.mask[:, 0, 0] == 0)
+    assert np.array_equal(f.U[:, 0, 0], u) and np.array_equal(f.vals[:, 0, 0], np.ones(4))
+    h16, c16 = oracle.run(f, b, x, [1], operand_round="bf16")
+    zeros = np.zeros((4, 3))
+    he, ce = oracle.exact_lstm(zeros, b + u * z16, x)
+    assert np.array_equal(h16[0], he) and np.array_equal(c16[0], ce)
+    h_unrounded, _ = oracle.exact_lstm(zeros, b + u * sig * x0, x)
+    h_late, _ = oracle.exact_lstm(zeros, oracle.round_bf16(b + u * sig * x0), x)
+    assert not np.array_equal(h16[0], h_unrounded)
+    assert not np.array_equal(h16[0], h_late)
+
+
 def test_termination_and_degenerate_zero_matrix():
     """A zero gate matrix has no live terms (every sigma 0, output bias-only)."""
     D, H = 6, 2
