@@ -152,6 +152,32 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
                                    int32_t n_levels, float* h_out, float* c_out, void* hip_stream);
 
 /*
+ * approx_lstm_run_noalloc -- approx_lstm_run for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results and kernels as
+ * approx_lstm_run for an fp32 model (bitwise the same outputs), but the run
+ * workspace (x-part projections, exchange words, bulk h buffers and flags)
+ * lives in one static device array of 32 MiB per device, held until the
+ * process ends; the call itself calls no hipMalloc, hipFree or other
+ * allocating routine (the model's factor store and error word were allocated
+ * by approx_lstm_prepare).  The first call on a device looks up the array's
+ * address there (hipGetSymbolAddress).
+ *
+ * Limits and errors: UNSUPPORTED when the run's workspace exceeds 32 MiB
+ * (about G*K*T*B*4 bytes of x-part projections plus the exchange words; the
+ * message gives the size), for bf16 models and for T > 65534; otherwise as
+ * approx_lstm_run.  No timing stamps are recorded.
+ *
+ * Concurrency: every call on one device shares that device's array; calls
+ * whose work overlaps on one device (different streams, or different host
+ * threads without ordering) race on it and must be serialised by the caller.
+ * Calls on one stream are ordered and safe.
+ */
+approx_lstm_status approx_lstm_run_noalloc(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                           const float* h0, const float* c0, const int32_t* levels,
+                                           int32_t n_levels, float* h_out, float* c_out, void* hip_stream);
+
+/*
  * approx_lstm_run_deadline -- progressive LSTM under a per-timestep time
  * budget (the paper's time-constrained setting: the best output reachable
  * within the budget, Sec. I, and computation cut when the budget is hit,

@@ -64,6 +64,7 @@ _sigs = {
     "approx_lstm_run_deadline": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
     "approx_lstm_run_anytime": [_vp, _vp, _i32, _i32, _vp, _vp, ctypes.c_double, _vp, _vp, _vp, _vp],
     "approx_lstm_run_schedule": [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp],
+    "approx_lstm_run_noalloc": [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp],
     "approx_lstm_plan": [_vp, _i32, _i32, _vp, _i32, _i32, _i32, _vp],
     "approx_lstm_check": [_vp, _vp],
     "approx_lstm_set_launch": [_vp, _i32, _i32],
@@ -165,6 +166,19 @@ def approx_lstm_run(model, x, levels, h_out, h0=None, c0=None, c_out=None, strea
     st = lib.approx_lstm_run(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)), _dev(c0, "c0", (B, H)),
                              lv, len(levels), _dev(h_out, "h_out", (len(levels), T, B, H)),
                              _dev(c_out, "c_out", (len(levels), B, H)), ctypes.c_void_p(_stream(stream)))
+    return _check(st)
+
+
+def approx_lstm_run_noalloc(model, x, levels, h_out, h0=None, c0=None, c_out=None, stream=None):
+    """As approx_lstm_run, with the workspace in the library's static device
+    scratch (no allocation in the call)."""
+    T, B, D = x.shape
+    lv = (ctypes.c_int32 * len(levels))(*[int(k) for k in levels])
+    H = model.hidden_size
+    st = lib.approx_lstm_run_noalloc(model.handle, _dev(x, "x"), T, B, _dev(h0, "h0", (B, H)),
+                                     _dev(c0, "c0", (B, H)), lv, len(levels),
+                                     _dev(h_out, "h_out", (len(levels), T, B, H)),
+                                     _dev(c_out, "c_out", (len(levels), B, H)), ctypes.c_void_p(_stream(stream)))
     return _check(st)
 
 

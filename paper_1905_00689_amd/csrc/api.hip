@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <thread>
@@ -439,11 +440,43 @@ size_t plan_run(const approx_lstm_model* m, alstm::RunArgs& a, int32_t T, int32_
   return lds;
 }
 
+// Byte layout of a run's workspace carved from one caller-side region (the
+// allocation-free entry point): P_x, z words, h words, bulk h, flags, each
+// aligned to 256 bytes.
+struct ScratchLayout {
+  size_t px, zx, hx, hbx, hflag, total;
+};
+
+ScratchLayout scratch_layout(size_t px_floats, size_t zx_words, size_t hx_words, size_t hbx_floats, size_t flags) {
+  ScratchLayout l{};
+  size_t o = 0;
+  l.px = o;    o = round_up(o + 4 * px_floats, 256);
+  l.zx = o;    o = round_up(o + 8 * zx_words, 256);
+  l.hx = o;    o = round_up(o + 8 * hx_words, 256);
+  l.hbx = o;   o = round_up(o + 4 * hbx_floats, 256);
+  l.hflag = o; o = round_up(o + 4 * flags, 256);
+  l.total = o;
+  return l;
+}
+
+// Workspace handed in by the allocation-free entry point: `base` (device,
+// 256-byte aligned) holds `bytes`; launch tags come from `seq` (per device),
+// and the exchange words of the region are cleared whenever it wraps.
+struct CallerScratch {
+  unsigned char* base;
+  size_t bytes;
+  unsigned* seq;
+};
+
 // The fp32 progressive run (argument checks done by the caller): fixed
-// levels, or with `on` one online level sized for kmax.
+// levels, or with `on` one online level sized for kmax.  With `ws` the
+// workspace is carved from the caller's region (nothing is allocated; no
+// timing stamps), otherwise it is the model's own, grown on demand.
 approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t T, int32_t B, const float* h0,
                                    const float* c0, const int32_t* levels, int32_t n_levels, int kmax, float* h_out,
-                                   float* c_out, hipStream_t stream, const OnlineCfg* on) {
+                                   float* c_out, hipStream_t stream, const OnlineCfg* on,
+                                   const CallerScratch* ws = nullptr) {
+  if (on && ws) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "online runs need the model's own workspace");
   alstm::RunArgs a{};
   int P = 1;
   const size_t lds = plan_run(m, a, T, B, levels, n_levels, kmax, on, m->num_cu, &P);
@@ -455,34 +488,62 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
   const size_t kword = on ? 1 : 0;   // K_t of an online run rides with h
   // h words per step parity (tagged words in hx, floats in the bulk hbx)
   a.hb_stride = (int)round_up(LB * m->H + kword, 4);
-  approx_lstm_status st =
-      ensure_workspace(m, std::max<size_t>(1, (size_t)a.GK * T * B), std::max<size_t>(1, LB * P * a.owned_max),
-                       2 * (size_t)a.hb_stride, stream);
-  if (st != APPROX_LSTM_OK) return st;
   a.bulk_h = alstm::use_bulk_h(n_levels, B, m->H);
-  if (a.bulk_h) {
-    st = ensure_bulk(m, 2 * (size_t)a.hb_stride, stream);
+  const size_t px_floats = std::max<size_t>(1, (size_t)a.GK * T * B);
+  const size_t zx_words = std::max<size_t>(1, LB * P * a.owned_max);
+  const size_t hx_words = 2 * (size_t)a.hb_stride;
+  unsigned tag_seq = 0;
+  if (ws) {
+    const ScratchLayout sl = scratch_layout(px_floats, zx_words, hx_words, a.bulk_h ? hx_words : 0, (size_t)P);
+    if (sl.total > ws->bytes)
+      return fail(APPROX_LSTM_ERR_UNSUPPORTED,
+                  "run needs %zu bytes of workspace, above the %zu-byte static scratch of the allocation-free entry "
+                  "point (T=%d, B=%d, levels=%d, G*K=%d)",
+                  sl.total, ws->bytes, T, B, n_levels, a.GK);
+    a.px = reinterpret_cast<float*>(ws->base + sl.px);
+    a.zx = reinterpret_cast<unsigned long long*>(ws->base + sl.zx);
+    a.hx = reinterpret_cast<unsigned long long*>(ws->base + sl.hx);
+    a.hbx = a.bulk_h ? reinterpret_cast<float*>(ws->base + sl.hbx) : nullptr;
+    a.hflag = a.bulk_h ? reinterpret_cast<unsigned*>(ws->base + sl.hflag) : nullptr;
+    *ws->seq = (*ws->seq + 1) & 0xFFFFu;
+    if (*ws->seq == 0) {
+      // tag space wrapped: clear every exchange word of the region (a fill
+      // kernel) so no stale tag can match
+      const size_t words = (ws->bytes - sl.zx) / 8;
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(ws->base + sl.zx), words, stream),
+              "clear(scratch)");
+      *ws->seq = 1;
+    }
+    tag_seq = *ws->seq;
+  } else {
+    approx_lstm_status st = ensure_workspace(m, px_floats, zx_words, hx_words, stream);
     if (st != APPROX_LSTM_OK) return st;
+    if (a.bulk_h) {
+      st = ensure_bulk(m, hx_words, stream);
+      if (st != APPROX_LSTM_OK) return st;
+    }
+    m->seq = (m->seq + 1) & 0xFFFFu;
+    if (m->seq == 0) {
+      // tag space wrapped: clear the exchange words so no stale tag can match
+      HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
+      HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+      if (m->d_hflag)
+        HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
+                "clear(hflag)");
+      m->seq = 1;
+    }
+    tag_seq = m->seq;
+    a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx;
+    a.hbx = a.bulk_h ? m->d_hbx : nullptr;
+    a.hflag = a.bulk_h ? m->d_hflag : nullptr;
   }
-  m->seq = (m->seq + 1) & 0xFFFFu;
-  if (m->seq == 0) {
-    // tag space wrapped: clear the exchange words so no stale tag can match
-    HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
-    HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
-    if (m->d_hflag)
-      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
-              "clear(hflag)");
-    m->seq = 1;
-  }
-  a.tag_base = m->seq << 16;
+  a.tag_base = tag_seq << 16;
   a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
   a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
   a.sigma = m->d_sigma; a.Ut = m->d_Ut; a.vidx = m->d_vidx; a.vval = m->d_vval; a.nx = m->d_nx;
-  a.bias = m->d_bias; a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx; a.err = m->d_err;
-  a.hbx = a.bulk_h ? m->d_hbx : nullptr;
-  a.hflag = a.bulk_h ? m->d_hflag : nullptr;
+  a.bias = m->d_bias; a.err = m->d_err;
   a.stamps = nullptr;
-  if (m->timing) {
+  if (m->timing && !ws) {
     const size_t words = 4 + 4 * (size_t)T;
     if (words > m->stamps_cap) {
       HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
@@ -507,6 +568,27 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
   HIP_TRY(alstm::launch_progressive(a, P, m->cooperative, stream), "launch progressive_lstm_kernel");
   return APPROX_LSTM_OK;
 }
+
+}  // namespace
+
+// Workspace of approx_lstm_run_noalloc (callers that cannot allocate): one
+// array on every device the library runs on, held until the process ends.
+// In host code this name is only a host-side stand-in: the array's device
+// address is taken once per device with hipGetSymbolAddress and only that
+// address is used (kernel arguments, fills).  Every call on a device shares
+// its array, which keeps the last call's contents.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+struct ScratchSlot {
+  unsigned char* ptr = nullptr;   // device address of `scratch` on this device
+  unsigned seq = 0;               // launch tags of the calls using it
+};
+std::mutex g_scratch_mu;
+ScratchSlot g_scratch_slot[kMaxScratchDevices];
 
 }  // namespace
 
@@ -703,6 +785,10 @@ approx_lstm_status approx_lstm_prepare(const float* w_ih, const float* w_hh, con
       up(m->d_vidx, vi_h.data(), vi_h.size() * 2, "vidx");
       up(m->d_nx, nx_h.data(), NT * 2, "nx");
     }
+    // the device-side error word, cleared once here: runs (including those
+    // that may not allocate) only set it, approx_lstm_check reads and clears it
+    if (st == APPROX_LSTM_OK) step(hipMalloc(&m->d_err, 64), "hipMalloc(err)");
+    if (st == APPROX_LSTM_OK) step(hipMemsetAsync(m->d_err, 0, 64, stream), "clear(err)");
     if (st == APPROX_LSTM_OK) step(hipStreamSynchronize(stream), "hipStreamSynchronize");
     if (st != APPROX_LSTM_OK) {
       delete m;
@@ -768,6 +854,46 @@ approx_lstm_status approx_lstm_run(approx_lstm_model* m, const float* x, int32_t
   if (m->dtype == 1) return run_batched(m, x, T, B, h0, c0, levels, n_levels, h_out, c_out, stream);
 
   return run_progressive(m, x, T, B, h0, c0, levels, n_levels, kmax, h_out, c_out, stream, nullptr);
+}
+
+approx_lstm_status approx_lstm_run_noalloc(approx_lstm_model* m, const float* x, int32_t T, int32_t B,
+                                           const float* h0, const float* c0, const int32_t* levels,
+                                           int32_t n_levels, float* h_out, float* c_out, void* hip_stream) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (!m->has_dev) return fail(APPROX_LSTM_ERR_INVALID_ARG, "model has no device store (HOST_ONLY)");
+  if (m->dtype != 0) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "the allocation-free run takes fp32 models only");
+  if (T < 0 || B < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need T >= 0 and B >= 1");
+  if (T > 65534) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "T = %d exceeds 65534", T);
+  if (!levels || n_levels < 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "need at least one level");
+  if (n_levels > APPROX_LSTM_MAX_LEVELS)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "at most %d levels per run", APPROX_LSTM_MAX_LEVELS);
+  int kmax = 0;
+  for (int l = 0; l < n_levels; ++l) {
+    if (levels[l] < 0 || levels[l] > m->N)
+      return fail(APPROX_LSTM_ERR_INVALID_ARG, "level %d: K = %d not in [0, %d]", l, levels[l], m->N);
+    kmax = std::max(kmax, (int)levels[l]);
+  }
+  if (T == 0) return APPROX_LSTM_OK;
+  if (!x || !h_out) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null x or h_out");
+  if (m->device < 0 || m->device >= kMaxScratchDevices)
+    return fail(APPROX_LSTM_ERR_UNSUPPORTED, "device %d beyond the %d the scratch registry holds", m->device,
+                kMaxScratchDevices);
+  DeviceScope ds(m->device);
+  if (!ds.ok) return fail(APPROX_LSTM_ERR_DEVICE, "cannot select the model's device");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  ScratchSlot& slot = g_scratch_slot[m->device];
+  if (!slot.ptr) {
+    // first call on this device (current): the array's address on it
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(APPROX_LSTM_ERR_DEVICE, "hipGetSymbolAddress(scratch) returned null");
+    slot.ptr = static_cast<unsigned char*>(p);
+  }
+  const CallerScratch ws{slot.ptr, kScratchBytes, &slot.seq};
+  return run_progressive(m, x, T, B, h0, c0, levels, n_levels, kmax, h_out, c_out, (hipStream_t)hip_stream,
+                         nullptr, &ws);
 }
 
 approx_lstm_status approx_lstm_run_stack(approx_lstm_model* const* layers, int32_t n_layers, const float* x, int32_t T,
