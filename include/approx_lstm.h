@@ -266,12 +266,14 @@ approx_lstm_status approx_lstm_run_schedule(approx_lstm_model* m, const float* x
  *                      (ignored when online != 0: the plan of an anytime or
  *                      scheduled run sized for the whole rank)
  *   num_cu             compute units to plan for (0 = the model's device)
- *   out                host [8]: workgroups, all-timestep P_x resident in LDS
+ *   out                host [9]: workgroups, all-timestep P_x resident in LDS
  *                      (1/0), all (level, sequence) pairs in one phase-B pass
  *                      (1/0), h-part entries per lane in registers, U entries
  *                      per thread in registers, output rows per thread, bulk
  *                      h exchange (1/0), LDS bytes per workgroup (above
- *                      163840: the run returns UNSUPPORTED)
+ *                      163840: the run returns UNSUPPORTED), and 1 when the
+ *                      run takes the one-pair recurrence kernel (see
+ *                      approx_lstm_set_recurrence), else 0
  *
  * Works on HOST_ONLY models.  Errors: INVALID_ARG for bad sizes or levels;
  * UNSUPPORTED for bf16 models.
@@ -329,6 +331,20 @@ approx_lstm_status approx_lstm_check(approx_lstm_model* m, void* hip_stream);
  * ignored there.
  */
 approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks, int32_t cooperative);
+
+/*
+ * approx_lstm_set_recurrence -- recurrence kernel of an fp32 model's fixed-
+ * budget runs, from the next run on.  kernel = 0 (the default): a run of one
+ * level over one sequence (approx_lstm_run with n_levels = 1 and B = 1, and
+ * the runs approx_lstm_run_deadline and approx_lstm_run_stack make of that
+ * form) takes the one-pair kernel where its launch plan fits (every owned
+ * h-part entry and U entry in registers: at most 2048 terms per
+ * sequence in use, K <= 1024, and the entries per lane it needs), every other
+ * run the general persistent kernel; kernel = 1: the general kernel always.
+ * Both compute every sum in the same order: the outputs are bitwise equal.
+ * Errors: null model, kernel not 0 or 1.
+ */
+approx_lstm_status approx_lstm_set_recurrence(approx_lstm_model* m, int32_t kernel);
 
 /*
  * approx_lstm_set_batched_path -- kernels of a bf16 model's recurrence (Eq. (1)

@@ -69,6 +69,7 @@ _sigs = {
     "approx_lstm_check": [_vp, _vp],
     "approx_lstm_set_launch": [_vp, _i32, _i32],
     "approx_lstm_set_batched_path": [_vp, _i32],
+    "approx_lstm_set_recurrence": [_vp, _i32],
     "approx_lstm_model_info": [_vp, ctypes.POINTER(Info)],
     "approx_lstm_set_timing": [_vp, _i32],
     "approx_lstm_get_timing": [_vp, _vp, _vp, _i32],
@@ -223,14 +224,14 @@ def approx_lstm_run_schedule(model, x, k_sched, h_out, h0=None, c0=None, c_out=N
     return _check(st)
 
 
-PLAN_FIELDS = ("blocks", "px_all", "allpairs", "hpl", "upt", "opt", "bulk_h", "lds_bytes")
+PLAN_FIELDS = ("blocks", "px_all", "allpairs", "hpl", "upt", "opt", "bulk_h", "lds_bytes", "pair_kernel")
 
 
 def approx_lstm_plan(model, T, B, levels=None, online=0, num_cu=0):
     """Launch plan of an fp32 run (no device work): dict of PLAN_FIELDS."""
     lv = levels if levels is not None else [0]
     arr, ap = _host(lv, np.int32)
-    out = np.zeros(8, np.int32)
+    out = np.zeros(9, np.int32)
     _check(lib.approx_lstm_plan(model.handle, T, B, ap, len(arr), int(online), int(num_cu), out.ctypes.data))
     return dict(zip(PLAN_FIELDS, (int(v) for v in out)))
 
@@ -260,6 +261,10 @@ def approx_lstm_check(model, stream=None):
 
 def approx_lstm_set_launch(model, blocks, cooperative=0):
     return _check(lib.approx_lstm_set_launch(model.handle, int(blocks), int(cooperative)))
+
+
+def approx_lstm_set_recurrence(model, kernel):
+    return _check(lib.approx_lstm_set_recurrence(model.handle, int(kernel)))
 
 
 def approx_lstm_set_batched_path(model, persistent):

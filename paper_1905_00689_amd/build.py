@@ -37,7 +37,7 @@ def _run(cmd, verbose):
     return r
 
 
-HIP_SOURCES = ("kernels.hip", "batched.hip", "exact.hip", "factorise_device.hip", "api.hip")
+HIP_SOURCES = ("kernels.hip", "kernels_pair.hip", "batched.hip", "exact.hip", "factorise_device.hip", "api.hip")
 
 
 def build(verbose=False):

@@ -133,6 +133,7 @@ struct approx_lstm_model {
   size_t kt_cap = 0;
   int launch_blocks = 0;             // 0 = automatic
   int cooperative = 0;               // 1: cooperative launch API
+  int recurrence = 0;                // 0: one-pair kernel where it applies, 1: general kernel only
   // persistent batched recurrence (bf16 models): cohort exchange buffers
   int batched_persistent = 1;        // 0: per-timestep kernel pairs only; 1: persistent where it
                                      // fits; 2, 3: persistent with z always tagged / always flagged
@@ -468,6 +469,105 @@ struct CallerScratch {
   unsigned* seq;
 };
 
+// Launch tag sequence of the next run: the model's own counter, or the
+// caller workspace's; on wrap the exchange words are cleared (fill kernels)
+// so that no stale tag can match.
+approx_lstm_status next_tag(approx_lstm_model* m, const CallerScratch* ws, size_t ws_exchange_offset,
+                            hipStream_t stream, unsigned* tag_seq) {
+  if (ws) {
+    *ws->seq = (*ws->seq + 1) & 0xFFFFu;
+    if (*ws->seq == 0) {
+      const size_t words = (ws->bytes - ws_exchange_offset) / 8;
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(ws->base + ws_exchange_offset), words,
+                                      stream),
+              "clear(scratch)");
+      *ws->seq = 1;
+    }
+    *tag_seq = *ws->seq;
+    return APPROX_LSTM_OK;
+  }
+  m->seq = (m->seq + 1) & 0xFFFFu;
+  if (m->seq == 0) {
+    HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
+    HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
+    if (m->d_hflag)
+      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
+              "clear(hflag)");
+    m->seq = 1;
+  }
+  *tag_seq = m->seq;
+  return APPROX_LSTM_OK;
+}
+
+approx_lstm_status ensure_stamps(approx_lstm_model* m, int T, hipStream_t stream) {
+  const size_t words = 4 + 4 * (size_t)T;
+  if (words > m->stamps_cap) {
+    HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    dfree(m->d_stamps);
+    m->stamps_cap = 0;
+    HIP_TRY(hipMalloc(&m->d_stamps, words * 8), "hipMalloc(stamps)");
+    m->stamps_cap = words;
+  }
+  m->last_T = T;
+  return APPROX_LSTM_OK;
+}
+
+// Plan of a one-pair run (one level, one sequence, K >= 1): P > 0 when the
+// one-pair kernel takes it.
+int plan_pair_run(const approx_lstm_model* m, alstm::PairArgs& pa, int T, int K, int num_cu, size_t* lds) {
+  pa = alstm::PairArgs{};
+  pa.D = m->D; pa.H = m->H; pa.G = m->G; pa.N = m->N; pa.NZ = m->NZ; pa.T = T;
+  pa.K = K; pa.GK = m->G * K;
+  pa.hcap = m->hpre[pa.GK - 1];
+  return alstm::plan_pair(pa, num_cu, m->launch_blocks, lds);
+}
+
+// One (level, sequence) pair on the one-pair kernel (P workgroups from
+// plan_pair_run): input projection, then the recurrence.
+approx_lstm_status run_pair(approx_lstm_model* m, alstm::PairArgs& pa, int P, const float* x, int32_t T,
+                            const float* h0, const float* c0, float* h_out, float* c_out, hipStream_t stream,
+                            const CallerScratch* ws) {
+  const size_t px_floats = (size_t)pa.GK * T, zx_words = (size_t)P * pa.OM, hx_words = round_up(m->H, 4);
+  size_t exch_off = 0;
+  float* pxw = nullptr;   // x-part projections: written by the input projection, read by the recurrence
+  if (ws) {
+    const ScratchLayout sl = scratch_layout(px_floats, zx_words, hx_words, 0, 0);
+    if (sl.total > ws->bytes)
+      return fail(APPROX_LSTM_ERR_UNSUPPORTED,
+                  "run needs %zu bytes of workspace, above the %zu-byte static scratch of the allocation-free entry "
+                  "point (T=%d, B=1, G*K=%d)",
+                  sl.total, ws->bytes, T, pa.GK);
+    pa.zx = reinterpret_cast<unsigned long long*>(ws->base + sl.zx);
+    pa.hx = reinterpret_cast<unsigned long long*>(ws->base + sl.hx);
+    pxw = reinterpret_cast<float*>(ws->base + sl.px);
+    exch_off = sl.zx;
+  } else {
+    approx_lstm_status st = ensure_workspace(m, px_floats, zx_words, hx_words, stream);
+    if (st != APPROX_LSTM_OK) return st;
+    pa.zx = m->d_zx; pa.hx = m->d_hx; pxw = m->d_px;
+  }
+  pa.px = pxw;
+  unsigned tag_seq = 0;
+  approx_lstm_status st = next_tag(m, ws, exch_off, stream, &tag_seq);
+  if (st != APPROX_LSTM_OK) return st;
+  pa.tag_base = tag_seq << 16;
+  pa.stamps = nullptr;
+  if (m->timing && !ws) {
+    st = ensure_stamps(m, T, stream);
+    if (st != APPROX_LSTM_OK) return st;
+    pa.stamps = m->d_stamps;
+  }
+  pa.h0 = h0; pa.c0 = c0; pa.h_out = h_out; pa.c_out = c_out;
+  pa.sigma = m->d_sigma; pa.Ut = m->d_Ut; pa.vidx = m->d_vidx; pa.vval = m->d_vval; pa.nx = m->d_nx;
+  pa.bias = m->d_bias; pa.err = m->d_err;
+  alstm::RunArgs proj{};
+  proj.x = x; proj.D = m->D; proj.NZ = m->NZ; proj.T = T; proj.B = 1; proj.GK = pa.GK;
+  proj.vidx = m->d_vidx; proj.vval = m->d_vval; proj.nx = m->d_nx; proj.px = pxw;
+  proj.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
+  HIP_TRY(alstm::launch_pair(proj, pa, P, stream), "launch pair_lstm_kernel");
+  return APPROX_LSTM_OK;
+}
+
 // The fp32 progressive run (argument checks done by the caller): fixed
 // levels, or with `on` one online level sized for kmax.  With `ws` the
 // workspace is carved from the caller's region (nothing is allocated; no
@@ -477,6 +577,12 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
                                    float* c_out, hipStream_t stream, const OnlineCfg* on,
                                    const CallerScratch* ws = nullptr) {
   if (on && ws) return fail(APPROX_LSTM_ERR_UNSUPPORTED, "online runs need the model's own workspace");
+  if (!on && n_levels == 1 && B == 1 && kmax > 0 && m->recurrence == 0 && !m->cooperative) {
+    alstm::PairArgs pa{};
+    size_t plds = 0;
+    const int Pp = plan_pair_run(m, pa, T, kmax, m->num_cu, &plds);
+    if (Pp > 0) return run_pair(m, pa, Pp, x, T, h0, c0, h_out, c_out, stream, ws);
+  }
   alstm::RunArgs a{};
   int P = 1;
   const size_t lds = plan_run(m, a, T, B, levels, n_levels, kmax, on, m->num_cu, &P);
@@ -493,6 +599,7 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
   const size_t zx_words = std::max<size_t>(1, LB * P * a.owned_max);
   const size_t hx_words = 2 * (size_t)a.hb_stride;
   unsigned tag_seq = 0;
+  size_t exch_off = 0;
   if (ws) {
     const ScratchLayout sl = scratch_layout(px_floats, zx_words, hx_words, a.bulk_h ? hx_words : 0, (size_t)P);
     if (sl.total > ws->bytes)
@@ -505,16 +612,7 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
     a.hx = reinterpret_cast<unsigned long long*>(ws->base + sl.hx);
     a.hbx = a.bulk_h ? reinterpret_cast<float*>(ws->base + sl.hbx) : nullptr;
     a.hflag = a.bulk_h ? reinterpret_cast<unsigned*>(ws->base + sl.hflag) : nullptr;
-    *ws->seq = (*ws->seq + 1) & 0xFFFFu;
-    if (*ws->seq == 0) {
-      // tag space wrapped: clear every exchange word of the region (a fill
-      // kernel) so no stale tag can match
-      const size_t words = (ws->bytes - sl.zx) / 8;
-      HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(ws->base + sl.zx), words, stream),
-              "clear(scratch)");
-      *ws->seq = 1;
-    }
-    tag_seq = *ws->seq;
+    exch_off = sl.zx;
   } else {
     approx_lstm_status st = ensure_workspace(m, px_floats, zx_words, hx_words, stream);
     if (st != APPROX_LSTM_OK) return st;
@@ -522,20 +620,13 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
       st = ensure_bulk(m, hx_words, stream);
       if (st != APPROX_LSTM_OK) return st;
     }
-    m->seq = (m->seq + 1) & 0xFFFFu;
-    if (m->seq == 0) {
-      // tag space wrapped: clear the exchange words so no stale tag can match
-      HIP_TRY(alstm::launch_clear_u64(m->d_zx, m->zx_cap, stream), "clear(zx)");
-      HIP_TRY(alstm::launch_clear_u64(m->d_hx, m->hx_cap, stream), "clear(hx)");
-      if (m->d_hflag)
-        HIP_TRY(alstm::launch_clear_u64(reinterpret_cast<unsigned long long*>(m->d_hflag), m->hflag_cap / 2, stream),
-                "clear(hflag)");
-      m->seq = 1;
-    }
-    tag_seq = m->seq;
     a.px = m->d_px; a.zx = m->d_zx; a.hx = m->d_hx;
     a.hbx = a.bulk_h ? m->d_hbx : nullptr;
     a.hflag = a.bulk_h ? m->d_hflag : nullptr;
+  }
+  {
+    approx_lstm_status st = next_tag(m, ws, exch_off, stream, &tag_seq);
+    if (st != APPROX_LSTM_OK) return st;
   }
   a.tag_base = tag_seq << 16;
   a.x = x; a.h0 = h0; a.c0 = c0; a.h_out = h_out; a.c_out = c_out;
@@ -544,16 +635,9 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
   a.bias = m->d_bias; a.err = m->d_err;
   a.stamps = nullptr;
   if (m->timing && !ws) {
-    const size_t words = 4 + 4 * (size_t)T;
-    if (words > m->stamps_cap) {
-      HIP_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
-      dfree(m->d_stamps);
-      m->stamps_cap = 0;
-      HIP_TRY(hipMalloc(&m->d_stamps, words * 8), "hipMalloc(stamps)");
-      m->stamps_cap = words;
-    }
+    approx_lstm_status st = ensure_stamps(m, T, stream);
+    if (st != APPROX_LSTM_OK) return st;
     a.stamps = m->d_stamps;
-    m->last_T = T;
   }
   if (on) {
     if ((size_t)T > m->kt_cap) {
@@ -986,6 +1070,14 @@ approx_lstm_status approx_lstm_set_launch(approx_lstm_model* m, int32_t blocks, 
   return APPROX_LSTM_OK;
 }
 
+approx_lstm_status approx_lstm_set_recurrence(approx_lstm_model* m, int32_t kernel) {
+  g_last_error.clear();
+  if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
+  if (kernel < 0 || kernel > 1) return fail(APPROX_LSTM_ERR_INVALID_ARG, "kernel must be 0 or 1");
+  m->recurrence = kernel;
+  return APPROX_LSTM_OK;
+}
+
 approx_lstm_status approx_lstm_set_batched_path(approx_lstm_model* m, int32_t persistent) {
   g_last_error.clear();
   if (!m) return fail(APPROX_LSTM_ERR_INVALID_ARG, "null model");
@@ -1234,13 +1326,29 @@ approx_lstm_status approx_lstm_plan(const approx_lstm_model* m, int32_t T, int32
       lv.push_back(levels[l]);
     }
   }
+  const int ncu = num_cu > 0 ? num_cu : m->num_cu;
+  for (int i = 0; i < 9; ++i) out[i] = 0;
+  if (!online && lv.size() == 1 && B == 1 && kmax > 0 && m->recurrence == 0 && !m->cooperative) {
+    alstm::PairArgs pa{};
+    size_t plds = 0;
+    const int Pp = plan_pair_run(m, pa, T, kmax, ncu, &plds);
+    if (Pp > 0) {
+      out[0] = Pp;
+      out[1] = pa.px_lds;
+      out[3] = pa.hpl;
+      out[4] = pa.upt;
+      out[5] = pa.opt;
+      out[7] = (int32_t)plds;
+      out[8] = 1;
+      return APPROX_LSTM_OK;
+    }
+  }
   OnlineCfg cfg;
   cfg.n = 1;
   cfg.k[0] = kmax;
   alstm::RunArgs a{};
   int P = 1;
-  const size_t lds = plan_run(m, a, T, B, lv.data(), (int)lv.size(), kmax, online ? &cfg : nullptr,
-                              num_cu > 0 ? num_cu : m->num_cu, &P);
+  const size_t lds = plan_run(m, a, T, B, lv.data(), (int)lv.size(), kmax, online ? &cfg : nullptr, ncu, &P);
   out[0] = P;
   out[1] = a.px_all;
   out[2] = a.allpairs;

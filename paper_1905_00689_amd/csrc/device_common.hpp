@@ -198,7 +198,21 @@ __device__ __forceinline__ float sigmoid_fast(float z) {
 }
 
 __device__ __forceinline__ float tanh_fast(float x) {
-  return 2.0f * sigmoid_fast(2.0f * x) - 1.0f;
+  return __builtin_fmaf(2.0f, sigmoid_fast(2.0f * x), -1.0f);
+}
+
+// The cell update of Sec. II from the four gate pre-activations (rows i, f,
+// g, o): c' = sigmoid(y_f) c + sigmoid(y_i) tanh(y_g), h = sigmoid(y_o)
+// tanh(c').  Every kernel takes it from here, with its one fused
+// multiply-add written out, so that the rounding never depends on how a
+// kernel's surrounding code lets the compiler contract the expression.
+__device__ __forceinline__ void cell_update(float yi, float yf, float yg, float yo, float& c, float& h) {
+  const float gi = sigmoid_fast(yi);
+  const float gf = sigmoid_fast(yf);
+  const float gg = tanh_fast(yg);
+  const float go = sigmoid_fast(yo);
+  c = __builtin_fmaf(gf, c, gi * gg);
+  h = go * tanh_fast(c);
 }
 
 }  // namespace

@@ -262,12 +262,8 @@ __global__ void __launch_bounds__(kThreads) exact_lstm_kernel(ExactArgs a) {
     for (int i = threadIdx.x; i < B * rc; i += kThreads) {
       const int b = i / rc, rr = i - b * rc;
       const float* y = ys + b * 4 * RP;
-      const float gi = sigmoid_fast(y[0 * rc + rr]);
-      const float gf = sigmoid_fast(y[1 * rc + rr]);
-      const float gg = tanh_fast(y[2 * rc + rr]);
-      const float go = sigmoid_fast(y[3 * rc + rr]);
-      const float c = gf * cs[b * RP + rr] + gi * gg;
-      const float hv = go * tanh_fast(c);
+      float c = cs[b * RP + rr], hv;
+      cell_update(y[0 * rc + rr], y[1 * rc + rr], y[2 * rc + rr], y[3 * rc + rr], c, hv);
       cs[b * RP + rr] = c;
       hown[b * RP + rr] = hv;
       if (local) hs[(size_t)b * H + r0 + rr] = hv;

@@ -449,12 +449,8 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
       if (stamp) a.stamps[4 + 4 * t] = clock64();
       for (int i = threadIdx.x; i < LB * rc; i += kThreads) {
         const int lb = i / rc, rr = i - lb * rc;
-        const float gi = sigmoid_fast(bs[0 * RP + rr]);
-        const float gf = sigmoid_fast(bs[1 * RP + rr]);
-        const float gg = tanh_fast(bs[2 * RP + rr]);
-        const float go = sigmoid_fast(bs[3 * RP + rr]);
-        const float c = gf * cs[lb * RP + rr] + gi * gg;
-        const float hv2 = go * tanh_fast(c);
+        float c = cs[lb * RP + rr], hv2;
+        cell_update(bs[0 * RP + rr], bs[1 * RP + rr], bs[2 * RP + rr], bs[3 * RP + rr], c, hv2);
         cs[lb * RP + rr] = c;
         hown[lb * RP + rr] = hv2;
         if (local) hs[lb * H + r0 + rr] = hv2;
@@ -515,12 +511,8 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
         };
         // gates and the c/h update of owned unit rr of pair lb
         auto cell = [&](const float* yl, int lb, int rr) {
-          const float gi = sigmoid_fast(yl[0 * RP + rr]);
-          const float gf = sigmoid_fast(yl[1 * RP + rr]);
-          const float gg = tanh_fast(yl[2 * RP + rr]);
-          const float go = sigmoid_fast(yl[3 * RP + rr]);
-          const float c = gf * cs[lb * RP + rr] + gi * gg;
-          const float hv2 = go * tanh_fast(c);
+          float c = cs[lb * RP + rr], hv2;
+          cell_update(yl[0 * RP + rr], yl[1 * RP + rr], yl[2 * RP + rr], yl[3 * RP + rr], c, hv2);
           cs[lb * RP + rr] = c;
           hown[lb * RP + rr] = hv2;
           if (local) hs[lb * H + r0 + rr] = hv2;
@@ -611,12 +603,8 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
           }
           lds_barrier();
           for (int rr = threadIdx.x; rr < rc; rr += kThreads) {
-            const float gi = sigmoid_fast(ys[0 * RP + rr]);
-            const float gf = sigmoid_fast(ys[1 * RP + rr]);
-            const float gg = tanh_fast(ys[2 * RP + rr]);
-            const float go = sigmoid_fast(ys[3 * RP + rr]);
-            const float c = gf * cs[lb * RP + rr] + gi * gg;
-            const float hv2 = go * tanh_fast(c);
+            float c = cs[lb * RP + rr], hv2;
+            cell_update(ys[0 * RP + rr], ys[1 * RP + rr], ys[2 * RP + rr], ys[3 * RP + rr], c, hv2);
             cs[lb * RP + rr] = c;
             hown[lb * RP + rr] = hv2;
             if (local) hs[lb * H + r0 + rr] = hv2;
@@ -968,7 +956,7 @@ hipError_t launch_u(const RunArgs& a, int blocks, int cooperative, size_t lds, h
   return launch_one<HPL, 1, 0>(a, blocks, cooperative, lds, stream);
 }
 
-hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hipStream_t stream) {
+hipError_t launch_input_proj(const RunArgs& a, hipStream_t stream) {
   if (a.GK > 0) {
     // largest chunk of (t, b) pairs whose transposed x fits in LDS (odd row
     // stride: the lanes' rows fall in different banks)
@@ -993,9 +981,14 @@ hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hip
     const int gx = (a.GK + per_block - 1) / per_block;
     const int gy = column_slices(gx, (TB + xchunk - 1) / xchunk);
     input_proj_kernel<<<dim3(gx, gy), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    return hipGetLastError();
   }
+  return hipSuccess;
+}
+
+hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hipStream_t stream) {
+  hipError_t e = launch_input_proj(a, stream);
+  if (e != hipSuccess) return e;
   const size_t lds = layout_of(a, a.online).total;
   switch (a.hpl) {
     case 4: return launch_u<4>(a, blocks, cooperative, lds, stream);

@@ -122,6 +122,66 @@ inline int column_slices(int row_groups, int chunks) {
 // returns the LDS bytes the kernel then needs (> kLdsCap: does not fit).
 size_t plan_progressive(RunArgs& a, int P);
 
+// Launches, on `stream`, the x-part projections px[tau][t*B+b] of the first
+// a.GK terms (input_proj_kernel over the whole device; nothing when GK = 0).
+// Uses a.x, a.T, a.B, a.D, a.NZ, a.GK, a.vidx, a.vval, a.nx, a.px, a.xvec.
+hipError_t launch_input_proj(const RunArgs& a, hipStream_t stream);
+
+// One (level, sequence) pair: the recurrence of one budget K over one
+// sequence, with every owned slice in registers (pair_lstm_kernel).  The
+// summation order of every quantity is that of progressive_lstm_kernel (16
+// lanes per term in phase A, lanes_for_level(K) lanes per U row in phase B),
+// so both kernels give bitwise the same outputs.  Device pointers:
+//   px     [GK][T]              x-part projections (input_proj_kernel, B = 1)
+//   zx     [P*OM] u64           tagged z words, slot j*OM + i carries term j + i*P
+//   hx     [H] u64              tagged h words
+//   h_out  [T][H]               this level's outputs; c_out [H] or null
+struct PairArgs {
+  const float* h0;
+  const float* c0;
+  float* h_out;
+  float* c_out;
+  const float* sigma;
+  const float* Ut;
+  const uint16_t* vidx;
+  const float* vval;
+  const uint16_t* nx;
+  const float* bias;
+  const float* px;
+  unsigned long long* zx;
+  unsigned long long* hx;
+  unsigned* err;
+  unsigned long long* stamps;   // as RunArgs::stamps (workgroup 0), or null
+  int D, H, G, N, NZ, T;
+  int K;         // budget (terms per group), >= 1
+  int GK;        // G * K
+  int hcap;      // largest h-part entry count of the terms in use
+  // launch plan (plan_pair)
+  int OM;        // terms owned per workgroup (at most 32 * apass)
+  int RU;        // hidden units owned per workgroup
+  int apass;     // phase-A passes of 32 terms (1 or 2)
+  int hpl;       // h-part entries per lane held (register bucket: 4, 8, 12, 16, 24, 32)
+  int S, lgS;    // lanes per U row (lanes_for_level(K)) and its log2
+  int upt;       // U entries per row and lane in use: ceil(K / S)
+  int umax;      // U entries per row and lane held (register bucket: 8, 16, 32)
+  int opt;       // output rows per thread (1, 2, 4)
+  int kstride;   // LDS floats between the terms of consecutive lanes of a row
+  int zstride;   // LDS floats per group of z
+  int hpad;      // LDS floats of h (H rounded up to 4)
+  int px_lds;    // 1: P_x of every timestep staged in LDS (required)
+  unsigned tag_base;
+};
+
+// Launch shape of a pair run: fills the plan fields and returns the
+// workgroup count P (0: the shape does not fit this kernel) for `num_cu`
+// compute units, or checks a requested width (`want` > 0).  *lds receives
+// the LDS bytes per workgroup.
+int plan_pair(PairArgs& a, int num_cu, int want, size_t* lds);
+
+// Launches, on `stream`, the input projection (as launch_progressive) and the
+// one-pair recurrence with P workgroups.
+hipError_t launch_pair(const RunArgs& proj, const PairArgs& a, int P, hipStream_t stream);
+
 // Launches, on `stream`, the input projection over the whole device and then
 // the persistent recurrence kernel with `blocks` workgroups.  cooperative != 0
 // uses the cooperative launch API for the latter (co-residency checked by the

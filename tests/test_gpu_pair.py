@@ -1,0 +1,127 @@
+"""The one-pair recurrence kernel (one level, one sequence: the batch-1 run).
+
+It computes every sum in the order of the general persistent kernel, so on
+the same model and inputs the two must agree bit for bit, whatever the
+launch shape: one workgroup (z and h through LDS), two phase-A passes,
+two or four output rows per thread, 1 to 16 lanes per U row, 64 U entries per
+lane, dense v.  Every run is also checked against the oracle on the
+library's exported terms (fp32 bar)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1905_00689_amd import synth
+from paper_1905_00689_amd import binding as B
+
+from .gpu_helpers import exported_factors, prep, rel_err, run_gpu, say
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+
+def both(m, x, K, h0=None, c0=None, blocks=0):
+    """(pair-kernel h, c), (general-kernel h, c) of one level K."""
+    B.approx_lstm_set_launch(m, blocks, 0)
+    plan = B.approx_lstm_plan(m, x.shape[0], x.shape[1], [K])
+    assert plan["pair_kernel"] == 1, plan
+    hp, cp = run_gpu(m, x, [K], h0, c0, want_c=True)
+    B.approx_lstm_set_recurrence(m, 1)
+    try:
+        hg, cg = run_gpu(m, x, [K], h0, c0, want_c=True)
+    finally:
+        B.approx_lstm_set_recurrence(m, 0)
+        B.approx_lstm_set_launch(m, 0, 0)
+    return plan, (hp, cp), (hg, cg)
+
+
+def check(m, w, K, h0=None, c0=None, blocks=0, f=None):
+    plan, (hp, cp), (hg, cg) = both(m, w.x, K, h0, c0, blocks)
+    ho, co = oracle.run(f if f is not None else exported_factors(m), w.b, w.x, [K], h0, c0)
+    e = rel_err(hp, ho)
+    say(f"  K={K} plan {plan} rel err {e:.2e}")
+    assert np.array_equal(hp, hg) and np.array_equal(cp, cg), K
+    assert e < TOL, (K, e)
+    assert np.abs(cp - co).max() <= TOL * max(1.0, np.abs(co).max())
+
+
+@pytest.fixture(scope="module")
+def driving_p75():
+    w = synth.named("driving")
+    say("prepare driving p=0.75 rank 512")
+    return w, prep(w, 512, 0.75)
+
+
+@pytest.mark.parametrize("K", [1, 2, 8, 16, 32, 64, 128, 256, 384, 512])
+def test_pair_kernel_driving_every_shape(driving_p75, K):
+    w, m = driving_p75
+    say("driving p=0.75, one pair, K", K)
+    check(m, w, K)
+
+
+@pytest.mark.parametrize("blocks", [32, 64, 128])
+def test_pair_kernel_driving_launch_widths(driving_p75, blocks):
+    """K = 512 on 32 (two phase-A passes, two rows per thread), 64 and 128
+    workgroups: the same bits."""
+    w, m = driving_p75
+    say("driving K=512 on", blocks, "workgroups")
+    check(m, w, 512, blocks=blocks)
+
+
+def test_pair_kernel_initial_state_and_tiny_groupings():
+    w = synth.named("tiny")
+    rng = np.random.default_rng(21)
+    h0 = rng.normal(size=(1, 32)).astype(np.float32)
+    c0 = rng.normal(size=(1, 32)).astype(np.float32)
+    for G, rank in ((4, 32), (1, 96)):
+        m = prep(w, rank, 0.5, groups=G)
+        f = oracle.prepare(w.W, 32, rank, 48, groups=G)
+        for K in (1, 5, rank):
+            say("tiny G", G, "K", K, "with h0, c0")
+            check(m, w, K, h0, c0, f=f)
+
+
+def test_pair_kernel_dense_and_half_pruned():
+    """NZ = C (32 h-part entries per lane) and NZ = C/2 at the driving shape."""
+    w = synth.named("driving")
+    for p, Ks in ((0.0, (8, 512)), (0.5, (16, 512))):
+        say("prepare driving p", p)
+        m = prep(w, 512, p)
+        for K in Ks:
+            say("driving p", p, "K", K)
+            check(m, w, K)
+
+
+def test_pair_kernel_wide_layer():
+    """A layer at the stacked workload's width (D = 1024 -> H = 1024, rank
+    1024, 75% pruning): 16 hidden units per workgroup at K = 512; budgets
+    above 512 take the general kernel."""
+    w = synth.make(1024, 1024, 8, 1, index=47, xkind="relu")
+    say("prepare D=1024 H=1024 rank 1024 p=0.75")
+    m = prep(w, 1024, 0.75)
+    for K in (256, 512):
+        check(m, w, K)
+    assert B.approx_lstm_plan(m, 8, 1, [1024])["pair_kernel"] == 0
+
+
+def test_pair_kernel_deadline_and_noalloc_paths(driving_p75):
+    """Timed runs (stamps) and the allocation-free entry point take the same
+    kernel and give the same bits."""
+    w, m = driving_p75
+    x = torch.from_numpy(w.x).cuda()
+    h1 = torch.empty((1, w.T, 1, w.H), device="cuda")
+    h2 = torch.empty((1, w.T, 1, w.H), device="cuda")
+    B.approx_lstm_set_timing(m, 1)
+    try:
+        B.approx_lstm_run(m, x, [64], h1)
+        st = B.approx_lstm_get_timing(m, w.T)
+    finally:
+        B.approx_lstm_set_timing(m, 0)
+    B.approx_lstm_run_noalloc(m, x, [64], h2)
+    B.approx_lstm_check(m)
+    torch.cuda.synchronize()
+    assert np.array_equal(h1.cpu().numpy(), h2.cpu().numpy())
+    steps = np.diff(np.asarray(st)[1::4][: w.T + 1])
+    say("  stamps: per-timestep us", [round(float(v), 2) for v in steps])
+    assert np.all(steps > 0)
