@@ -39,12 +39,17 @@ __device__ __forceinline__ float group_sum_rt(float v, int S) {
   }
 }
 
-// Full-wave sum (input projection): 16-lane rows, then across the 4 rows.
+// Full-wave sum (input projection): 16-lane rows, then (r0 + r1) + (r2 + r3)
+// over the four row sums, read into scalar registers (v_readlane: no LDS
+// round trip, unlike a cross-row lane shuffle).  The result is uniform.
 __device__ __forceinline__ float wave_sum(float v) {
   v = group_sum<16>(v);
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
+  const int b = __builtin_bit_cast(int, v);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48));
+  return (r0 + r1) + (r2 + r3);
 }
 
 __device__ __forceinline__ void publish(unsigned long long* p, float v, unsigned tag) {

@@ -7,21 +7,24 @@
 // budget prefix is spread over all workgroups) and the hidden units
 // [j*RU, j*RU + RU).  Every slice it needs stays in registers for the whole
 // sequence: the h-part entries of its terms (16 lanes per term, hpl entries
-// per lane) and the U entries of its 4*RU gate rows (S lanes per row, upt
-// entries per lane, opt rows per thread).  Per timestep:
+// per lane, one or two passes) and the U entries of its 4*RU gate rows
+// (S lanes per row, upt entries per lane, one, two or four rows per thread).
+// P_x of every timestep (input_proj_kernel) is staged in LDS up front.
+// Per timestep:
 //   phase A  each term's lane group sums its h-part entries against h_{t-1}
 //            (LDS), reduces over its 16 lanes and forms z = sigma * (P_x + s);
-//            the lane holding z publishes it at once as a tagged word;
-//   z wait   every thread polls its share of the G*K z words into LDS;
+//   z        the last wave (the publisher) stores the workgroup's z as
+//            tagged words; waves 0-6 poll every workgroup's words into LDS;
 //   phase B  each row's lanes sum u * z over their terms and reduce; the four
 //            gate rows of a unit lie in one wave (rows gate-minor), so the
 //            unit's lane gathers them by lane shuffles and applies the gate
 //            nonlinearities and the c/h update with c held in a register;
-//            it writes h to h_out and publishes it as a tagged word;
-//   h wait   every thread polls its share of the H h words into LDS.
-// Two LDS barriers per timestep and no publisher wave: the lanes that compute
-// a value store it, and every wave polls.  With one workgroup nothing is
-// exchanged (z and h go through LDS).
+//   h        the publisher writes h to h_out and stores it as tagged words;
+//            waves 0-6 poll every unit's h into LDS.
+// The publisher only stores and the pollers only load: a wave's loads and
+// stores retire through one in-order counter, so a wave that polled after
+// storing would wait for its own stores' acknowledgements every round.
+// With one workgroup (P = 1) nothing is exchanged: z and h go through LDS.
 //
 // The order of every sum is that of progressive_lstm_kernel (phase A: entry
 // sla + 16k of the term's h part at lane sla, k ascending, then the 16-lane
@@ -90,12 +93,25 @@ constexpr int kMaxWords = 8;
 constexpr int kLdsStamps = 255;
 
 // LDS carve-up (floats): stamps [2 * (4 + 4 * kLdsStamps)] (8-byte aligned
-// at offset 0), h [hpad], z [G][zstride], z of the owned terms [OM], h of the
-// owned units [RU], P_x [T][OM]
+// at offset 0), P_x [T][OM], then h [hpad], z [G][zstride], z of the owned
+// terms [OM], h of the owned units [RU], and per wave the gate
+// pre-activations of its rows [opt][64 / S] (16-byte aligned).
 constexpr int kStampFloats = 2 * (4 + 4 * kLdsStamps);
-__host__ __device__ inline size_t pair_lds_floats(const PairArgs& a) {
-  return (size_t)kStampFloats + a.hpad + (size_t)a.G * a.zstride + a.OM + a.RU + (size_t)a.T * a.OM;
+struct PairLayout {
+  size_t px, hs, zs, zown, hown, ys, total;
+};
+__host__ __device__ inline PairLayout pair_layout(const PairArgs& a) {
+  PairLayout l;
+  l.px = kStampFloats;
+  l.hs = l.px + (((size_t)a.T * a.OM + 3) & ~(size_t)3);
+  l.zs = l.hs + a.hpad;
+  l.zown = l.zs + (size_t)a.G * a.zstride;
+  l.hown = l.zown + a.OM;
+  l.ys = (l.hown + a.RU + 3) & ~(size_t)3;   // 16-byte aligned
+  l.total = l.ys + (size_t)kWaves * a.opt * (64 / a.S);
+  return l;
 }
+__host__ __device__ inline size_t pair_lds_floats(const PairArgs& a) { return pair_layout(a).total; }
 
 // OPT output rows per thread with UMAX U entries each in registers, APASS
 // phase-A passes with HMAX h-part entries per lane each.  Every loop runs to
@@ -113,12 +129,14 @@ __global__ void __launch_bounds__(kThreads) pair_lstm_kernel(PairArgs a) {
   const int D = a.D, H = a.H, G = a.G, N = a.N, NZ = a.NZ, T = a.T, K = a.K, GK = a.GK;
   const int OM = a.OM, RU = a.RU, zst = a.zstride, kst = a.kstride;
   const bool local = P == 1;
+  const PairLayout lay = pair_layout(a);
+  float* ldsf = reinterpret_cast<float*>(lds_raw);
   unsigned long long* lstamp = reinterpret_cast<unsigned long long*>(lds_raw);
-  float* hs = reinterpret_cast<float*>(lds_raw) + kStampFloats;   // h_{t-1} [H]
-  float* zs = hs + a.hpad;                          // z of this timestep [G][zst]
-  float* zown = zs + (size_t)G * zst;               // z of the owned terms [OM]
-  float* hown = zown + OM;                          // h of the owned units [RU]
-  float* pxs = hown + RU;                           // P_x [T][OM]
+  float* pxs = ldsf + lay.px;      // P_x [T][OM]
+  float* hs = ldsf + lay.hs;       // h_{t-1} [H]
+  float* zs = ldsf + lay.zs;       // z of this timestep [G][zst]
+  float* zown = ldsf + lay.zown;   // z of the owned terms [OM]
+  float* hown = ldsf + lay.hown;   // h of the owned units [RU]
   const int r0 = j * RU, rc = max(0, min(RU, H - r0));
   const int n_owned = GK > j ? (GK - j + P - 1) / P : 0;
   // uniform plan values, kept in scalar registers
@@ -127,12 +145,24 @@ __global__ void __launch_bounds__(kThreads) pair_lstm_kernel(PairArgs a) {
   // reads its terms sl + S*k at consecutive addresses (immediate offsets)
   auto zpos = [&](int tau) { const int g = tau % G, n = tau / G; return g * zst + (n & (S - 1)) * kst + (n >> lgS); };
 
+  // Prologue loads, ordered so that every independent load is in flight
+  // before the first wait: the first share of P_x and h0, sigma and the
+  // h/x split of the owned terms, the U entries, bias and c0; then the
+  // h-part entries (their addresses need the split).
+  const int npx = T * n_owned;
+  float px0 = 0.0f, h00 = 0.0f;
+  if (tid < npx) {
+    const int t0 = tid / n_owned, io0 = tid - t0 * n_owned;
+    px0 = a.px[(size_t)(j + io0 * P) * T + t0];
+  }
+  if (tid < H && a.h0) h00 = a.h0[tid];
+
   // ---- phase-A roles: lane group sub (16 lanes) takes owned terms sub + 32p
   const int sub = tid >> 4, sla = tid & 15;
   float hv[APASS][HMAX];
   int hi[APASS][HMAX];
   float sg[APASS];
-  int slot[APASS], zdst[APASS];
+  int slot[APASS], zdst[APASS], e0v[APASS];
 #pragma unroll
   for (int p = 0; p < APASS; ++p) {
     const int ia = sub + 32 * p;
@@ -141,8 +171,49 @@ __global__ void __launch_bounds__(kThreads) pair_lstm_kernel(PairArgs a) {
     sg[p] = own ? a.sigma[tau] : 0.0f;
     slot[p] = own ? j * OM + ia : -1;
     zdst[p] = own ? zpos(tau) : 0;
-    const int e0 = own ? (int)a.nx[tau] : 0, cnt = own ? NZ - e0 : 0;
-    const size_t src = (size_t)(own ? tau : 0) * NZ;
+    e0v[p] = own ? (int)a.nx[tau] : NZ;
+  }
+
+  // ---- phase-B roles: row slot rs = tid / S, rows rs + o * (512 / S); row ol
+  // is gate q = ol & 3 of owned unit ol >> 2 (gate-minor: a unit's four rows
+  // are four adjacent lane groups of one wave)
+  const int rs = tid >> lgS, sl = tid & (S - 1);
+  const int nslots = kThreads >> lgS;
+  float uv[OPT][UMAX];
+  float bq[OPT];
+  // every row of a thread has gate q = rs & 3 (row slots per pass are a
+  // multiple of 4): one z base for all of them
+  const int zb = (G == 4 ? (rs & 3) : 0) * zst + sl * kst;
+  // ---- cell roles: a wave holds the rows of 16 * OPT / S units (row slots
+  // [w * 64/S, (w+1) * 64/S) in each of the OPT passes); its lane cl takes
+  // unit cl, pass co = cl / (16/S), row slots 4 ck .. 4 ck + 3 (ck = cl %
+  // (16/S)), and keeps that unit's c in a register.  The rows' sums reach
+  // it through the wave's LDS block ysw[o][64/S] (no cross-wave traffic).
+  const int wv = tid >> 6, rpw = 64 >> lgS, upw = (16 * OPT) >> lgS;
+  const int co = lane / (16 >> lgS), ck = lane % (16 >> lgS);
+  const int cunit = (wv * rpw + 4 * ck + co * nslots) >> 2;
+  const bool cell_ok = lane < upw && cunit < rc;
+  float cst = (cell_ok && a.c0) ? a.c0[r0 + cunit] : 0.0f;
+  float* ysw = ldsf + lay.ys + (size_t)wv * OPT * rpw;
+#pragma unroll
+  for (int o = 0; o < OPT; ++o) {
+    const int ol = rs + o * nslots, ul = ol >> 2, q = ol & 3;
+    const bool rowv = ul < rc;
+    const size_t row = (size_t)q * H + r0 + ul;
+    bq[o] = rowv ? a.bias[row] : 0.0f;
+    const float* urow = a.Ut + (rowv ? row : 0) * N;
+#pragma unroll
+    for (int k = 0; k < UMAX; ++k) uv[o][k] = urow[min(sl + S * k, K - 1)];
+#pragma unroll
+    for (int k = 0; k < UMAX; ++k) uv[o][k] = (rowv && sl + S * k < K) ? uv[o][k] : 0.0f;
+  }
+
+#pragma unroll
+  for (int p = 0; p < APASS; ++p) {
+    const int ia = sub + 32 * p;
+    const int tau = ia < n_owned ? j + ia * P : 0;
+    const int e0 = e0v[p], cnt = NZ - e0;
+    const size_t src = (size_t)tau * NZ;
     // every load issued (index clamped into the term's entries), then masked
 #pragma unroll
     for (int k = 0; k < HMAX; ++k) {
@@ -154,36 +225,8 @@ __global__ void __launch_bounds__(kThreads) pair_lstm_kernel(PairArgs a) {
     for (int k = 0; k < HMAX; ++k) {
       const bool live = sla + 16 * k < cnt;
       hv[p][k] = live ? hv[p][k] : 0.0f;
-      hi[p][k] = 4 * kStampFloats + (live ? 4 * (hi[p][k] - D) : 0);   // byte offset of h[k - D] in LDS
+      hi[p][k] = 4 * (int)lay.hs + (live ? 4 * (hi[p][k] - D) : 0);   // byte offset of h[k - D] in LDS
     }
-  }
-
-  // ---- phase-B roles: row slot rs = tid / S, rows rs + o * (512 / S); row ol
-  // is gate q = ol & 3 of owned unit ol >> 2 (gate-minor: a unit's four rows
-  // are four adjacent lane groups of one wave)
-  const int rs = tid >> lgS, sl = tid & (S - 1);
-  const int nslots = kThreads >> lgS;
-  float uv[OPT][UMAX];
-  float bq[OPT], cst[OPT];
-  int unit[OPT];
-  bool cell[OPT];
-  // every row of a thread has gate q = rs & 3 (row slots per pass are a
-  // multiple of 4): one z base for all of them
-  const int zb = (G == 4 ? (rs & 3) : 0) * zst + sl * kst;
-#pragma unroll
-  for (int o = 0; o < OPT; ++o) {
-    const int ol = rs + o * nslots, ul = ol >> 2, q = ol & 3;
-    const bool rowv = ul < rc;
-    const size_t row = (size_t)q * H + r0 + ul;
-    unit[o] = ul;
-    bq[o] = rowv ? a.bias[row] : 0.0f;
-    cell[o] = rowv && q == 0 && sl == 0;
-    cst[o] = (cell[o] && a.c0) ? a.c0[r0 + ul] : 0.0f;
-    const float* urow = a.Ut + (rowv ? row : 0) * N;
-#pragma unroll
-    for (int k = 0; k < UMAX; ++k) uv[o][k] = urow[min(sl + S * k, K - 1)];
-#pragma unroll
-    for (int k = 0; k < UMAX; ++k) uv[o][k] = (rowv && sl + S * k < K) ? uv[o][k] : 0.0f;
   }
 
   // ---- exchange roles: z slots tid + 512 r (slot s = j'*OM + i' carries
@@ -203,11 +246,13 @@ __global__ void __launch_bounds__(kThreads) pair_lstm_kernel(PairArgs a) {
   }
 
   // ---- LDS: initial state, P_x of every timestep when it fits
-  for (int i = tid; i < H; i += kThreads) hs[i] = a.h0 ? a.h0[i] : 0.0f;
+  if (tid < H) hs[tid] = h00;
+  for (int i = tid + kThreads; i < H; i += kThreads) hs[i] = a.h0 ? a.h0[i] : 0.0f;
   // z slots of terms past the budget (n >= K in a lane's last entry) are
   // never written and must read 0 (their u entries are 0 as well)
   for (int i = tid; i < G * zst; i += kThreads) zs[i] = 0.0f;
-  for (int i = tid; i < T * n_owned; i += kThreads) {
+  if (tid < npx) pxs[(tid / n_owned) * OM + tid % n_owned] = px0;
+  for (int i = tid + kThreads; i < npx; i += kThreads) {
     const int t = i / n_owned, io = i - t * n_owned;
     pxs[t * OM + io] = a.px[(size_t)(j + io * P) * T + t];
   }
@@ -279,20 +324,25 @@ __global__ void __launch_bounds__(kThreads) pair_lstm_kernel(PairArgs a) {
     }
 #pragma unroll
     for (int o = 0; o < OPT; ++o) y[o] = group_sum_rt(acc[o], S) + bq[o];
+    // the rows' sums go to the wave's block (lane sl == 0 of each row), then
+    // each unit's lane reads its four gate rows at once and updates c and h
+    if (sl == 0) {
 #pragma unroll
-    for (int o = 0; o < OPT; ++o) {
-      // gate rows f, g, o of this unit sit S, 2S and 3S lanes up
-      const float yf = __shfl(y[o], lane + S, 64);
-      const float yg = __shfl(y[o], lane + 2 * S, 64);
-      const float yo = __shfl(y[o], lane + 3 * S, 64);
-      if (cell[o]) {
-        float h2;
-        cell_update(y[o], yf, yg, yo, cst[o], h2);
+      for (int o = 0; o < OPT; ++o) ysw[o * rpw + ((tid & 63) >> lgS)] = y[o];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < upw) {
+      const float4 g4 = *reinterpret_cast<const float4*>(ysw + co * rpw + 4 * ck);
+      float h2;
+      cell_update(g4.x, g4.y, g4.z, g4.w, cst, h2);
+      if (cell_ok) {
         if (local) {
-          hs[r0 + unit[o]] = h2;
-          a.h_out[(size_t)t * H + r0 + unit[o]] = h2;
+          hs[r0 + cunit] = h2;
+          a.h_out[(size_t)t * H + r0 + cunit] = h2;
         } else {
-          hown[unit[o]] = h2;
+          hown[cunit] = h2;
         }
       }
     }
@@ -317,11 +367,7 @@ __global__ void __launch_bounds__(kThreads) pair_lstm_kernel(PairArgs a) {
     if (st == lstamp)
       for (int i = 0; i < 4 + 4 * T; ++i) a.stamps[i] = lstamp[i];
   }
-  if (a.c_out) {
-#pragma unroll
-    for (int o = 0; o < OPT; ++o)
-      if (cell[o]) a.c_out[r0 + unit[o]] = cst[o];
-  }
+  if (a.c_out && cell_ok) a.c_out[r0 + cunit] = cst;
 }
 
 template <int OPT, int UMAX, int APASS, int HMAX>
@@ -357,9 +403,9 @@ int plan_pair(PairArgs& a, int num_cu, int want, size_t* lds) {
     const int opt = (4 * RU + slots - 1) / slots;
     const int opt_b = opt <= 1 ? 1 : (opt <= 2 ? 2 : (opt <= 4 ? 4 : 0));
     if (!opt_b || a.upt > 32 / (opt_b == 4 ? 2 : 1)) return false;
-    // register budget: two phase-A passes next to at most 16 h-part entries
-    // per lane, and four rows per thread next to 8
-    if (apass == 2 && (need_h > 16 || (opt_b == 4 && need_h > 8))) return false;
+    // register budget: two phase-A passes hold at most 16 h-part entries per
+    // lane (every instance fits its registers without spilling)
+    if (apass == 2 && need_h > 16) return false;
     // the four gate rows of a unit must be adjacent lane groups of one wave
     if (4 * a.S > 64) return false;
     if ((size_t)P * OM > (size_t)kMaxWords * kPollThreads || a.H > kMaxWords * kPollThreads) return false;
@@ -412,10 +458,8 @@ int plan_pair(PairArgs& a, int num_cu, int want, size_t* lds) {
 template <int APASS, int HMAX>
 hipError_t launch_pair_u(const PairArgs& a, int P, size_t lds, hipStream_t stream) {
   if (a.opt == 4) {
-    if constexpr (!(APASS == 2 && HMAX > 8)) {
-      if (a.umax == 8) return launch_pair_kernel<4, 8, APASS, HMAX>(a, P, lds, stream);
-      return launch_pair_kernel<4, 16, APASS, HMAX>(a, P, lds, stream);
-    }
+    if (a.umax == 8) return launch_pair_kernel<4, 8, APASS, HMAX>(a, P, lds, stream);
+    return launch_pair_kernel<4, 16, APASS, HMAX>(a, P, lds, stream);
   } else if (a.opt == 2) {
     if (a.umax == 16) return launch_pair_kernel<2, 16, APASS, HMAX>(a, P, lds, stream);
     return launch_pair_kernel<2, 32, APASS, HMAX>(a, P, lds, stream);

@@ -198,6 +198,18 @@ def test_driving_plan_of_the_timed_workload(driving, driving_full_p75):
     p = B.approx_lstm_plan(driving_full_p75, 16, 1, [512], num_cu=256)
     assert p["px_all"] == 1 and p["bulk_h"] == 0 and p["hpl"] > 0 and p["upt"] > 0, p
     assert p["lds_bytes"] <= 160 * 1024, p
+    assert p["pair_kernel"] == 1 and p["blocks"] > 1, p
+
+
+def test_driving_small_budgets_take_one_workgroup(driving_full_p75):
+    """Budgets up to K = 16 at the driving shape fit one workgroup's
+    registers (two phase-A passes, four output rows per thread): nothing is
+    exchanged between workgroups.  K = 32 needs more than one."""
+    for K in (1, 2, 4, 8, 16):
+        p = B.approx_lstm_plan(driving_full_p75, 16, 1, [K], num_cu=256)
+        assert p["pair_kernel"] == 1 and p["blocks"] == 1, (K, p)
+    p = B.approx_lstm_plan(driving_full_p75, 16, 1, [32], num_cu=256)
+    assert p["pair_kernel"] == 1 and p["blocks"] > 1, p
 
 
 def test_driving_no_pruning_gives_the_svd(driving):
