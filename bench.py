@@ -24,6 +24,11 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
+def progress(msg):
+    """One progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def algorithmic_bytes_per_timestep(G, Rg, NZ, C, K, D, H, B, L):
     """Bytes the method must move per timestep (Eq. (1) streamed once per
     timestep, as the paper's design streams u and v for every refinement):
@@ -54,6 +59,10 @@ def main():
     ap.add_argument("--no-anytime", action="store_true", help="skip the error-vs-time comparison with the row-tile baseline")
     ap.add_argument("--no-batched", action="store_true",
                     help="skip the batched (256 sequences, bf16 MFMA) summary in the default line")
+    ap.add_argument("--no-prune-sweep", action="store_true",
+                    help="skip the pruning sweep (0, 50, 90%% at K=512) in the default line")
+    ap.add_argument("--no-stack", action="store_true", help="skip the stacked-layer summary in the default line")
+    ap.add_argument("--no-deadline", action="store_true", help="skip the deadline-workload summary in the default line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only time a plain 256 MiB device copy (reference for HBM counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -124,6 +133,7 @@ def main():
         return e0.elapsed_time(e1) / steps   # ms per run
 
     K = args.K
+    progress(f"driving prepared ({prep_s:.1f} s); timing K={K}")
     ms = timed(K, args.steps, args.warmup)
     us_per_ts = ms * 1e3 / T
     value = T * Bn / (ms * 1e-3)
@@ -140,6 +150,7 @@ def main():
         sweep["timesteps_per_s"].append(round(T * Bn / (msk * 1e-3), 1))
         sweep["hbm_frac"].append(round(byts / (msk * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
 
+    progress("K sweep done")
     tune = None
     if args.blocks_sweep:
         tune = {"K": K, "blocks": [], "us_per_timestep": []}
@@ -164,16 +175,60 @@ def main():
                           "recurrence_us": round(float(st[1 + 4 * T] - st[1]), 3)}
 
     # One step launches input_proj_kernel (x-part projections, whole GPU) and
-    # then progressive_lstm_kernel (the recurrence); the roofline covers the
-    # step, timed with events on the launch stream over the timed region.
+    # then the recurrence (pair_lstm_kernel for one level of one sequence,
+    # else progressive_lstm_kernel); the roofline covers the step, timed with
+    # events on the launch stream over the timed region.
+    plan = B.approx_lstm_plan(m, T, Bn, [K])
+    rec = "pair_lstm_kernel" if plan["pair_kernel"] else "progressive_lstm_kernel"
     bytes_launch = T * algorithmic_bytes_per_timestep(G, Rg, NZ, C, K, D, H, Bn, 1)
     achieved = bytes_launch / (ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic("driving") if (K == 512 and abs(args.prune - 0.75) < 1e-9) else None,
-                "kernel": "one step: input_proj_kernel + progressive_lstm_kernel",
+                "kernel": f"one step: input_proj_kernel + {rec} ({plan['blocks']} workgroups)",
                 "bytes_per_launch": bytes_launch,
                 "flops_per_launch": T * algorithmic_flops_per_timestep(G, Rg, NZ, K, Bn)}
+
+    # the same step at the other pruning ratios of the driving configuration
+    # (factorised on the device), K = 512 and 64
+    progress("phases done")
+    prune_sweep = None
+    if not args.no_prune_sweep:
+        prune_sweep = {"prune": [], "nz": [], "prepare_device_s": [], "us_per_timestep_K512": [],
+                       "hbm_frac_K512": [], "us_per_timestep_K64": []}
+        for p in (0.0, 0.5, 0.75, 0.9):
+            if abs(p - args.prune) < 1e-9:
+                mp, sec = m, None
+            else:
+                t1 = time.time()
+                mp = B.approx_lstm_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H, rank, prune_ratio=p, groups=4,
+                                           flags=B.FLAG_DEVICE_FACTORISE)
+                sec = round(time.time() - t1, 2)
+            nzp = mp.info["nz"]
+            row = {}
+            for kk in (512, 64):
+                for _ in range(5):
+                    B.approx_lstm_run(mp, x, [kk], h_out, stream=stream)
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(args.sweep_steps):
+                    B.approx_lstm_run(mp, x, [kk], h_out, stream=stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                B.approx_lstm_check(mp)
+                row[kk] = e0.elapsed_time(e1) / args.sweep_steps
+            byts = T * algorithmic_bytes_per_timestep(G, Rg, nzp, C, 512, D, H, Bn, 1)
+            prune_sweep["prune"].append(p)
+            prune_sweep["nz"].append(nzp)
+            prune_sweep["prepare_device_s"].append(sec)
+            prune_sweep["us_per_timestep_K512"].append(round(row[512] * 1e3 / T, 4))
+            prune_sweep["hbm_frac_K512"].append(round(byts / (row[512] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+            prune_sweep["us_per_timestep_K64"].append(round(row[64] * 1e3 / T, 4))
+            if mp is not m:
+                del mp
+            progress(f"prune {p} done")
 
     # the exact (dense) LSTM on the same sequence, timed the same way: the
     # baseline the progressive approximation trades accuracy against
@@ -195,14 +250,22 @@ def main():
         return e0.elapsed_time(e1) / steps
 
     ms_exact = timed_exact(args.sweep_steps, 5)
+    progress("exact baseline done")
     exact = {"us_per_timestep": round(ms_exact * 1e3 / T, 4), "timesteps_per_s": round(T * Bn / (ms_exact * 1e-3), 1),
              "weights_bytes": 4 * 4 * H * (D + H)}
     anytime = None if args.no_anytime else anytime_comparison(torch, B, stream)
+    progress("anytime comparison done")
     batched = None if args.no_batched else batched_summary(args, torch)
+    progress("batched summary done")
+    stack = None if args.no_stack else stack_summary(args, torch)
+    progress("stack summary done")
+    deadline = None if args.no_deadline else deadline_summary(args, torch)
+    progress("deadline summary done")
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(m, wl, K, args.cpu_seconds)
+        progress("cpu baseline done")
 
     out = {
         "metric": "LSTM timesteps/sec at refinement budget K (and us/timestep vs K)",
@@ -213,8 +276,9 @@ def main():
                                f"{int(args.prune * 100)}% pruning (NZ={NZ}), K={K}",
                    "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": NZ, "K": K, "groups": G},
         "us_per_timestep": round(us_per_ts, 4), "step_ms": dist, "prepare_s": round(prep_s, 2),
-        "phases": phases, "sweep": sweep, "tune": tune, "exact_baseline": exact, "anytime": anytime,
-        "batched": batched, "roofline": roofline, "cpu_baseline": cpu,
+        "phases": phases, "sweep": sweep, "prune_sweep": prune_sweep, "tune": tune, "exact_baseline": exact,
+        "anytime": anytime, "batched": batched, "stack": stack, "deadline": deadline, "roofline": roofline,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 
@@ -349,7 +413,15 @@ def anytime_comparison(torch, B, stream):
     return out
 
 
-def bench_stack(args, torch):
+def stack_summary(args, torch):
+    """The stacked workload's budgets sweep, exact baseline and device
+    factorisation time, for the default line (full record: --workload stack)."""
+    out = bench_stack(args, torch, emit=False)
+    return {"workload": out["config"]["workload"], "prepare_device_s": out["prepare_device_s"],
+            "sweep": out["sweep"], "exact_baseline": out["exact_baseline"], "roofline": out["roofline"]}
+
+
+def bench_stack(args, torch, emit=True):
     """The stacked workload: layer 1 D=4096 -> H=1024, layer 2 1024 -> 1024,
     T=32, one sequence, fp32, per-layer rank 1024, 75% pruning (NZ = 1280 and
     512), factorised on the device.  A step is one approx_lstm_run_stack at one
@@ -369,6 +441,7 @@ def bench_stack(args, torch):
     m2 = B.approx_lstm_prepare(W2[:, :H], W2[:, H:], b2, H, H, rank, prune_ratio=0.75, groups=4,
                                flags=B.FLAG_DEVICE_FACTORISE)
     prep_s = time.time() - t0
+    progress(f"stack: both layers prepared on the device in {prep_s:.1f} s")
     nz1, nz2 = m1.info["nz"], m2.info["nz"]
     x = torch.from_numpy(wl.x).to(dev)
     stream = torch.cuda.current_stream()
@@ -432,27 +505,30 @@ def bench_stack(args, torch):
                            "timesteps_per_s": round(T * Bn / (ms_exact * 1e-3), 1)},
         "roofline": roofline, "cpu_baseline": None,
     }
-    print(json.dumps(out), flush=True)
+    if emit:
+        print(json.dumps(out), flush=True)
+    return out
 
 
-def bench_deadline(args, torch):
-    """The deadline workload (D=2048, H=2048, T=64, 8 sequences, per-gate rank
-    2048, 90% pruning, fp32).  The factorisation runs on the device; then
-    fixed budgets are timed, and both deadline modes run at 5, 20 and 100 us
-    per timestep: one K for the sequence (approx_lstm_run_deadline) and K_t
+def deadline_record(torch, name, steps=10):
+    """One weights model of the deadline workload (D=2048, H=2048, T=64, 8
+    sequences, per-gate rank 2048, 90% pruning, fp32), factorised on the
+    device: fixed budgets timed, then both deadline modes at 5, 20 and 100 us
+    per timestep, one K for the sequence (approx_lstm_run_deadline) and K_t
     chosen per timestep on the device (approx_lstm_run_anytime).  Each
     reports the budgets achieved, the measured step times and the output's
     error against the device's exact LSTM on the same input (see _qor)."""
     from paper_1905_00689_amd import synth
     from paper_1905_00689_amd import binding as B
     dev = torch.device("cuda")
-    wl = synth.named("deadline")
+    wl = synth.named(name)
     D, H, T, Bn = wl.D, wl.H, wl.T, wl.B
     rank = 2048
     t0 = time.time()
     m = B.approx_lstm_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H, rank, prune_ratio=0.9, groups=4,
                               flags=B.FLAG_DEVICE_FACTORISE)
     prep_s = time.time() - t0
+    progress(f"{name}: prepared on the device in {prep_s:.1f} s")
     x = torch.from_numpy(wl.x).to(dev)
     stream = torch.cuda.current_stream()
     me = B.approx_lstm_exact_prepare(wl.W[:, :D], wl.W[:, D:], wl.b, D, H)
@@ -462,7 +538,7 @@ def bench_deadline(args, torch):
     B.approx_lstm_exact_check(me)
     quality = _qor(synth.softmax_head(H).astype(np.float64), href.cpu().numpy().astype(np.float64))
 
-    def timed(fn, steps=10):
+    def timed(fn):
         fn()
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
@@ -488,7 +564,7 @@ def bench_deadline(args, torch):
 
     modes = {}
     h = torch.empty((T, Bn, H), device=dev)
-    for name, fn in (("one_K", B.approx_lstm_run_deadline), ("anytime", B.approx_lstm_run_anytime)):
+    for mode, fn in (("one_K", B.approx_lstm_run_deadline), ("anytime", B.approx_lstm_run_anytime)):
         rows = []
         for dl in (5.0, 20.0, 100.0):
             try:
@@ -504,16 +580,36 @@ def bench_deadline(args, torch):
                          "step_us_mean": round(float(np.mean(us)), 3), "step_us_max": round(float(np.max(us)), 3),
                          "steps_within_deadline": round(float(np.mean(us <= dl)), 3),
                          "rel_err": _sig(e), "kl": _sig(kl)})
-        modes[name] = rows
-    value = T * Bn / (fixed["us_per_timestep"][-1] * 1e-6 * T)
+        modes[mode] = rows
+    return {"weights": "gaussian" if name == "deadline" else "decaying spectrum", "nz": m.info["nz"],
+            "prepare_device_s": round(prep_s, 2), "fixed_budgets": fixed,
+            "exact_us_per_timestep": round(ms_exact * 1e3 / T, 3), "deadline_modes": modes}
+
+
+def deadline_summary(args, torch):
+    """Both weights models of the deadline workload, for the default line."""
+    return {"workload": "deadline: D=2048 H=2048 T=64 B=8, per-gate rank 2048, 90% pruning",
+            "gaussian": deadline_record(torch, "deadline", steps=5),
+            "decay": deadline_record(torch, "deadline-decay", steps=5),
+            "note": "errors against the device's exact LSTM; 'steps_within_deadline' is the share of timesteps "
+                    "whose measured time met the deadline"}
+
+
+def bench_deadline(args, torch):
+    """The deadline workload on Gaussian weights (flat spectrum: every budget
+    short of full rank leaves a large error) and on decaying-spectrum weights
+    (where the refinement order pays off)."""
+    g = deadline_record(torch, "deadline")
+    d = deadline_record(torch, "deadline-decay")
+    T, Bn = 64, 8
+    value = T * Bn / (g["fixed_budgets"]["us_per_timestep"][-1] * 1e-6 * T)
     out = {
         "metric": "deadline mode: achieved K, step time and error vs the exact LSTM at per-timestep deadlines",
         "value": round(value, 1), "unit": "timesteps/s at K=2048", "n_gpus": 1, "higher_is_better": True,
         "dtype": "f32", "data": "synthetic",
-        "config": {"workload": "deadline: D=2048 H=2048 T=64 B=8, per-gate rank 2048, 90% pruning (NZ=410)",
-                   "D": D, "H": H, "T": T, "batch": Bn, "rank": rank, "nz": m.info["nz"]},
-        "prepare_device_s": round(prep_s, 2), "fixed_budgets": fixed,
-        "exact_us_per_timestep": round(ms_exact * 1e3 / T, 3), "deadline_modes": modes,
+        "config": {"workload": f"deadline: D=2048 H=2048 T=64 B=8, per-gate rank 2048, 90% pruning (NZ={g['nz']})",
+                   "D": 2048, "H": 2048, "T": T, "batch": Bn, "rank": 2048, "nz": g["nz"]},
+        "gaussian": g, "decay": d,
         "note": "errors against the device's exact LSTM; 'steps_within_deadline' is the share of timesteps "
                 "whose measured time met the deadline",
     }
@@ -614,6 +710,7 @@ def bench_batched(args, torch, emit=True, step_dist=True):
         return e0.elapsed_time(e1) / steps
 
     K = args.K
+    progress(f"driving prepared ({prep_s:.1f} s); timing K={K}")
     ms = timed(K, args.steps, args.warmup)
     dist = (step_distribution(torch, lambda: B.approx_lstm_run(m, x, [K], h_out, stream=stream), stream, args.steps)
             if step_dist else None)
@@ -697,6 +794,18 @@ def oracle_threads():
         return os.cpu_count()
 
 
+def blas_info():
+    """The BLAS NumPy calls (library, version, threading layer, threads)."""
+    try:
+        from threadpoolctl import threadpool_info
+        libs = [d for d in threadpool_info() if d.get("user_api") == "blas"]
+        return [{"library": d.get("internal_api"), "version": d.get("version"),
+                 "threading_layer": d.get("threading_layer"), "threads": d.get("num_threads"),
+                 "file": os.path.basename(d.get("filepath", ""))} for d in libs]
+    except Exception as exc:
+        return [{"error": str(exc)}]
+
+
 TRAFFIC_PROFILES = {
     "driving": ("driving_K512_p75_hbm_counters.md", ("kernels.hip", "kernels.hpp", "device_common.hpp")),
     "batched": ("batched_K512_p75_hbm_counters.md", ("batched.hip", "kernels.hpp", "device_common.hpp")),
@@ -778,17 +887,30 @@ def cpu_baseline(m, wl, K, seconds):
             "sample": f"oracle.run (float64 NumPy) over the full T={wl.T} sequence at K={K}, "
                       f"repeated {runs} times ({el:.1f} s), on the library's exported terms",
             "single_thread_value": None if single is None else round(single, 2),
-            "exact_lstm_value": round(exact, 2), "cpu_model": cpu_model()}
+            "exact_lstm_value": round(exact, 2), "cpu_model": cpu_model(), "blas": blas_info(),
+            "host_cpus": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
 def cpu_model():
+    """The host CPU as /proc/cpuinfo names it: model name, vendor, family /
+    model / stepping (the name alone can be a generic string in a VM)."""
+    info = {}
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+            if ":" not in line:
+                continue
+            k, v = (t.strip() for t in line.split(":", 1))
+            if k in ("model name", "vendor_id", "cpu family", "model", "stepping", "cpu MHz", "cache size") \
+                    and k not in info:
+                info[k] = v
+            if not line.strip():
+                break
     except OSError:
-        pass
-    return None
+        return None
+    name = info.get("model name")
+    return {"name": name, "vendor": info.get("vendor_id"), "family": info.get("cpu family"),
+            "model": info.get("model"), "stepping": info.get("stepping"), "cache": info.get("cache size"),
+            "mhz": info.get("cpu MHz")}
 
 
 if __name__ == "__main__":

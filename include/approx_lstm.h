@@ -266,14 +266,16 @@ approx_lstm_status approx_lstm_run_schedule(approx_lstm_model* m, const float* x
  *                      (ignored when online != 0: the plan of an anytime or
  *                      scheduled run sized for the whole rank)
  *   num_cu             compute units to plan for (0 = the model's device)
- *   out                host [9]: workgroups, all-timestep P_x resident in LDS
+ *   out                host [10]: workgroups, all-timestep P_x resident in LDS
  *                      (1/0), all (level, sequence) pairs in one phase-B pass
  *                      (1/0), h-part entries per lane in registers, U entries
  *                      per thread in registers, output rows per thread, bulk
  *                      h exchange (1/0), LDS bytes per workgroup (above
- *                      163840: the run returns UNSUPPORTED), and 1 when the
- *                      run takes the one-pair recurrence kernel (see
- *                      approx_lstm_set_recurrence), else 0
+ *                      163840: the run returns UNSUPPORTED), 1 when the run
+ *                      takes the one-pair recurrence kernel (see
+ *                      approx_lstm_set_recurrence), else 0, and the K tile of
+ *                      a phase B that reads each U entry once per timestep
+ *                      for every sequence (0: one pass per sequence)
  *
  * Works on HOST_ONLY models.  Errors: INVALID_ARG for bad sizes or levels;
  * UNSUPPORTED for bf16 models.

@@ -224,14 +224,15 @@ def approx_lstm_run_schedule(model, x, k_sched, h_out, h0=None, c0=None, c_out=N
     return _check(st)
 
 
-PLAN_FIELDS = ("blocks", "px_all", "allpairs", "hpl", "upt", "opt", "bulk_h", "lds_bytes", "pair_kernel")
+PLAN_FIELDS = ("blocks", "px_all", "allpairs", "hpl", "upt", "opt", "bulk_h", "lds_bytes", "pair_kernel",
+               "ktile")
 
 
 def approx_lstm_plan(model, T, B, levels=None, online=0, num_cu=0):
     """Launch plan of an fp32 run (no device work): dict of PLAN_FIELDS."""
     lv = levels if levels is not None else [0]
     arr, ap = _host(lv, np.int32)
-    out = np.zeros(9, np.int32)
+    out = np.zeros(len(PLAN_FIELDS), np.int32)
     _check(lib.approx_lstm_plan(model.handle, T, B, ap, len(arr), int(online), int(num_cu), out.ctypes.data))
     return dict(zip(PLAN_FIELDS, (int(v) for v in out)))
 

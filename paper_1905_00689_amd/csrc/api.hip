@@ -414,6 +414,7 @@ size_t plan_run(const approx_lstm_model* m, alstm::RunArgs& a, int32_t T, int32_
   a = alstm::RunArgs{};
   a.D = m->D; a.H = m->H; a.G = m->G; a.N = m->N; a.NZ = m->NZ; a.T = T; a.B = B; a.L = n_levels;
   a.GK = m->G * kmax;
+  a.num_cu = num_cu;
   for (int l = 0; l < n_levels; ++l) a.levels[l] = levels[l];
   if (on) {
     // one level sized for the largest budget; the kernel takes K_t per timestep
@@ -564,6 +565,7 @@ approx_lstm_status run_pair(approx_lstm_model* m, alstm::PairArgs& pa, int P, co
   proj.x = x; proj.D = m->D; proj.NZ = m->NZ; proj.T = T; proj.B = 1; proj.GK = pa.GK;
   proj.vidx = m->d_vidx; proj.vval = m->d_vval; proj.nx = m->d_nx; proj.px = pxw;
   proj.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
+  proj.num_cu = m->num_cu;
   HIP_TRY(alstm::launch_pair(proj, pa, P, stream), "launch pair_lstm_kernel");
   return APPROX_LSTM_OK;
 }
@@ -1327,7 +1329,7 @@ approx_lstm_status approx_lstm_plan(const approx_lstm_model* m, int32_t T, int32
     }
   }
   const int ncu = num_cu > 0 ? num_cu : m->num_cu;
-  for (int i = 0; i < 9; ++i) out[i] = 0;
+  for (int i = 0; i < 10; ++i) out[i] = 0;
   if (!online && lv.size() == 1 && B == 1 && kmax > 0 && m->recurrence == 0 && !m->cooperative) {
     alstm::PairArgs pa{};
     size_t plds = 0;
@@ -1357,6 +1359,7 @@ approx_lstm_status approx_lstm_plan(const approx_lstm_model* m, int32_t T, int32
   out[5] = a.opt;
   out[6] = alstm::use_bulk_h((int)lv.size(), B, m->H);
   out[7] = (int32_t)std::min<size_t>(lds, 0x7fffffff);
+  out[9] = a.ktile;
   return APPROX_LSTM_OK;
 }
 

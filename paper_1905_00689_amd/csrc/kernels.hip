@@ -167,6 +167,68 @@ __device__ void gather_every_pair(float* zs, const uint16_t* slot_term, const un
   }
 }
 
+// z gather of one tile of terms, [G*k0, G*(k0+kn)), for every (level,
+// sequence) pair of a one-level launch.  The K-tiled launch publishes z in
+// term order (word tau of the pair's block of P*OM words), so a tile's words
+// are contiguous.  The nthr gathering threads split into LB groups of
+// tpp = nthr / LB, one per pair; thread t of pair lb's group takes the
+// tile's terms G*k0 + t + tpp*k (k < NS), whose z land at
+// zt[(lb*G + tau % G)*KT + tau / G - k0].  Every load is issued at once and
+// only the words still missing are loaded again (after the first tile every
+// word has usually arrived: one load round trip per tile).  Bounded like
+// gather_level.
+template <int NS>
+__device__ void gather_tile(float* zt, const unsigned long long* src, int P, int OM, int LB, int G, int k0, int kn,
+                            int KT, unsigned tag, unsigned* err, int tid, int nthr) {
+  const int tpp = nthr / LB, lb = tid / tpp, t = tid - lb * tpp;
+  if (lb >= LB) return;
+  const int per = G * kn;
+  const unsigned long long* sp = src + (size_t)lb * P * OM + G * k0 + t;
+  float* zl = zt + (size_t)lb * G * KT;
+  unsigned pending = 0;
+#pragma unroll
+  for (int k = 0; k < NS; ++k)
+    if (t + tpp * k < per) pending |= 1u << k;
+  unsigned spins = 0;
+  while (pending) {
+    unsigned long long w[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k)
+      if ((pending >> k) & 1u) w[k] = load_tagged(sp + tpp * k);
+#pragma unroll
+    for (int k = 0; k < NS; ++k)
+      if (((pending >> k) & 1u) && (unsigned)(w[k] >> 32) == tag) {
+        const int r = t + tpp * k;   // term G*k0 + r: group r % G, index k0 + r / G
+        const int g = G == 4 ? (r & 3) : r % G, nl = G == 4 ? (r >> 2) : r / G;
+        zl[g * KT + nl] = __uint_as_float((unsigned)w[k]);
+        pending &= ~(1u << k);
+      }
+    if (pending && (++spins & 255u) == 0u &&
+        (spins >= kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+      __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+      for (int k = 0; k < NS; ++k)
+        if ((pending >> k) & 1u) {
+          const int r = t + tpp * k;
+          zl[(r % G) * KT + r / G] = 0.0f;
+        }
+      break;
+    }
+  }
+}
+
+// words per thread: the planner keeps a tile within kTileWords words per
+// thread of a pair's group
+__device__ __forceinline__ void gather_tile_any(float* zt, const unsigned long long* src, int P, int OM, int LB, int G,
+                                                int k0, int kn, int KT, unsigned tag, unsigned* err, int tid,
+                                                int nthr) {
+  const int tpp = nthr / LB;
+  const int per = (G * kn + tpp - 1) / tpp;
+  if (per <= 4) gather_tile<4>(zt, src, P, OM, LB, G, k0, kn, KT, tag, err, tid, nthr);
+  else if (per <= 8) gather_tile<8>(zt, src, P, OM, LB, G, k0, kn, KT, tag, err, tid, nthr);
+  else gather_tile<kTileWords>(zt, src, P, OM, LB, G, k0, kn, KT, tag, err, tid, nthr);
+}
+
 // LDS carve-up shared by the host planner and the kernel (byte offsets).
 struct Layout {
   size_t zs, hs, ys, bs, cs, zown, hown, sig, pxb, zmap, hval, hidx, us, total;
@@ -180,10 +242,13 @@ __host__ __device__ inline Layout layout_of(const RunArgs& a, int online) {
   const size_t kmax = a.G > 0 ? (size_t)a.GK / a.G : 0;
   size_t o = 0;
   // z of one (level, seq), [g][Kmax]; a single workgroup keeps every pair's
-  l.zs = o;     o = align16(o + 4 * ((a.P == 1 || a.allpairs) ? LB : 1) * (a.GK > 1 ? (size_t)a.GK : 1));
+  // (a K-tiled phase B holds one tile of every pair's z instead)
+  const size_t zfl = ((a.P == 1 || a.allpairs) ? LB : 1) * (a.GK > 1 ? (size_t)a.GK : 1);
+  const size_t ztl = a.ktile > 0 ? LB * a.G * (size_t)a.ktile : 0;
+  l.zs = o;     o = align16(o + 4 * (zfl > ztl ? zfl : ztl));
   // h_{t-1} per (level, seq); an online run receives K_t in one more slot
   l.hs = o;     o = align16(o + 4 * (LB * a.H + (online ? 1 : 0)));
-  l.ys = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per * (a.allpairs ? LB : 1));   // y of the owned rows
+  l.ys = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per * ((a.allpairs || a.ktile > 0) ? LB : 1));   // y of the owned rows
   l.bs = o;     o = align16(o + 4 * 4 * (size_t)a.rows_per);          // bias of the owned rows
   l.cs = o;     o = align16(o + 4 * LB * a.rows_per);                 // c of the owned rows
   l.zown = o;   o = align16(o + 4 * LB * (size_t)a.owned_max);        // z of the owned terms
@@ -209,7 +274,7 @@ __host__ __device__ inline Layout layout_of(const RunArgs& a, int online) {
 // 4*rows_per*S <= 512*OPT); 0: U rows in LDS (ustride > 0) or from global.
 // ONLINE: one level whose budget is chosen per timestep (RunArgs::online);
 // the fixed-budget kernels carry none of its code.
-template <int HPL, int OPT, int UPT, bool ONLINE, bool AP>
+template <int HPL, int OPT, int UPT, bool ONLINE, bool AP, bool TILE>
 __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   const Layout L = layout_of(a, ONLINE ? 1 : 0);
@@ -437,7 +502,9 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
         const int GKl = G * (ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, lb / B));
         const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
         for (int i = lane; i < nl; i += 64)
-          publish(a.zx + (size_t)lb * P * OM + j * OM + i, zown[lb * OM + i], tag);
+          // slot j*OM + i, or (K-tiled phase B) word tau = j + i*P: a tile's
+          // terms are then contiguous words
+          publish(a.zx + (size_t)lb * P * OM + (a.ktile > 0 ? j + i * P : j * OM + i), zown[lb * OM + i], tag);
       }
     }
 
@@ -542,74 +609,143 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
         }
         lds_barrier();
       } else {
-        for (int lb = 0; lb < LB; ++lb) {
-          const int l = lb / B;
-          const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l);
-          if (!local && !publisher) {
-            // every slot of the exchange whose term is in this level (slots of
-            // workgroups that own fewer terms are skipped by the map check)
-            const int nslots = P * OM;
-            const int GKl = G * Kl;
-            gather_level_any(zs, zmap, a.zx + (size_t)lb * P * OM, nslots, GKl, G, Kmax, tag, a.err, threadIdx.x, gthr);
-          }
-          lds_barrier();
-          if (stamp && lb == 0) a.stamps[4 + 4 * t] = clock64();
-          const float* zl = zs + (local ? lb * GK : 0);
-          if constexpr (UPT > 0) {
-            // branch-free: entries past the budget multiply a valid z by 0
+        if constexpr (TILE) {
+          {
+            // One level over several sequences, U read from memory: each
+            // lane reads each of its U entries once per timestep and applies
+            // it to every sequence (one accumulator per pair and row), K in
+            // tiles of KT terms whose z of every pair are gathered into LDS
+            // (zs[(lb*G + g)*KT + n - k0]).  Per pair the sums run in the
+            // per-pair pass's order (entries sl, sl + S, ... ascending, then
+            // the S-lane reduction, then the bias).
+            const int KT = a.ktile;
+            const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, 0);
+            const int S = __builtin_amdgcn_readlane(vlanes, 0), lgS = 31 - __builtin_clz(S);
+            const int os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
+            // one output row per thread (the planner's condition)
+            float acc[kTilePairs];
+            const int ol = os;
+            const bool rv = ol < outs;
+            const int q = rv ? ol / rc : 0, rr0 = rv ? ol - q * rc : 0;
+            const float* urow = a.Ut + (size_t)(q * H + r0 + rr0) * N;
+            const int yq = q * RP + rr0, zq = ((G == 4) ? q : 0) * KT;
 #pragma unroll
-            for (int o = 0; o < OPT; ++o) {
-              // all z reads first (independent LDS loads in flight), then the FMAs
-              float zv[UPT];
+            for (int lb = 0; lb < kTilePairs; ++lb) acc[lb] = 0.0f;
+            for (int k0 = 0; k0 < Kl; k0 += KT) {
+              const int kn = min(KT, Kl - k0);
+              // the lane's U entries of the tile (KT <= kTileEntries * S), in
+              // registers before the gather so that their latency overlaps it
+              float ut[kTileEntries];
+              if (rv) {
 #pragma unroll
-              for (int k = 0; k < UPT; ++k) {
-                const int n = slb + S0 * k;
-                zv[k] = zl[zbase[o] + (n < Kl ? n : 0)];
+                for (int e = 0; e < kTileEntries; ++e) ut[e] = urow[min(k0 + sl + S * e, Kl - 1)];
               }
-              float acc = 0.0f;
+              if (k0 > 0) lds_barrier();   // every read of the previous tile is done
+              if (!publisher)
+                gather_tile_any(zs, a.zx, P, OM, LB, G, k0, kn, KT, tag, a.err, threadIdx.x, gthr);
+              lds_barrier();
+              if (stamp && k0 == 0) a.stamps[4 + 4 * t] = clock64();
+              if (rv) {
+                const float* zg = zs + zq - k0;
 #pragma unroll
-              for (int k = 0; k < UPT; ++k) {
-                const int n = slb + S0 * k;
-                acc += (n < Kl ? uv[o * UPT + k] : 0.0f) * zv[k];
-              }
-              acc = group_sum_rt(acc, S0);
-              if (yslot[o] >= 0 && slb == 0) ys[yslot[o]] = acc + bs[yslot[o]];
-            }
-          } else {
-            // S is a power of two (1 .. 16)
-            const int S = __builtin_amdgcn_readlane(vlanes, l), lgS = 31 - __builtin_clz(S);
-            const int OPP = kThreads >> lgS, os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
-            for (int base = 0; base < outs; base += OPP) {
-              const int ol = base + os;
-              float acc = 0.0f;
-              int q = 0, rr = 0;
-              if (ol < outs) {
-                q = ol / rc;
-                rr = ol - q * rc;
-                const float* zg = zl + ((G == 4) ? q : 0) * Kmax;
-                if (a.ustride) {
-                  const float* urow = us + (size_t)(q * RP + rr) * a.ustride;
-#pragma unroll 8
-                  for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
-                } else {
-                  const float* urow = a.Ut + (size_t)(q * H + r0 + rr) * N;
-#pragma unroll 8
-                  for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+                for (int e = 0; e < kTileEntries; ++e) {
+                  const int n = k0 + sl + S * e;
+                  if (n < k0 + kn) {
+#pragma unroll
+                    for (int lb = 0; lb < kTilePairs; ++lb)
+                      if (lb < LB) acc[lb] += ut[e] * zg[lb * G * KT + n];
+                  }
                 }
               }
-              acc = group_sum_rt(acc, S);
-              if (sl == 0 && ol < outs) ys[q * RP + rr] = acc + bs[q * RP + rr];
             }
+#pragma unroll
+            for (int lb = 0; lb < kTilePairs; ++lb)
+              if (lb < LB) {
+                const float v = group_sum_rt(acc[lb], S);
+                if (sl == 0 && rv) ys[lb * 4 * RP + yq] = v + bs[yq];
+              }
+            lds_barrier();
+            for (int i = threadIdx.x; i < LB * rc; i += kThreads) {
+              const int lb = i / rc, rr = i - lb * rc;
+              const float* yl = ys + lb * 4 * RP;
+              float c = cs[lb * RP + rr], hv2;
+              cell_update(yl[0 * RP + rr], yl[1 * RP + rr], yl[2 * RP + rr], yl[3 * RP + rr], c, hv2);
+              cs[lb * RP + rr] = c;
+              hown[lb * RP + rr] = hv2;
+            }
+            lds_barrier();
           }
-          lds_barrier();
-          for (int rr = threadIdx.x; rr < rc; rr += kThreads) {
-            float c = cs[lb * RP + rr], hv2;
-            cell_update(ys[0 * RP + rr], ys[1 * RP + rr], ys[2 * RP + rr], ys[3 * RP + rr], c, hv2);
-            cs[lb * RP + rr] = c;
-            hown[lb * RP + rr] = hv2;
-            if (local) hs[lb * H + r0 + rr] = hv2;
+        } else {
+          for (int lb = 0; lb < LB; ++lb) {
+            const int l = lb / B;
+            const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, l);
+            if (!local && !publisher) {
+              // every slot of the exchange whose term is in this level (slots of
+              // workgroups that own fewer terms are skipped by the map check)
+              const int nslots = P * OM;
+              const int GKl = G * Kl;
+              gather_level_any(zs, zmap, a.zx + (size_t)lb * P * OM, nslots, GKl, G, Kmax, tag, a.err, threadIdx.x, gthr);
+            }
+            lds_barrier();
+            if (stamp && lb == 0) a.stamps[4 + 4 * t] = clock64();
+            const float* zl = zs + (local ? lb * GK : 0);
+            if constexpr (UPT > 0) {
+              // branch-free: entries past the budget multiply a valid z by 0
+  #pragma unroll
+              for (int o = 0; o < OPT; ++o) {
+                // all z reads first (independent LDS loads in flight), then the FMAs
+                float zv[UPT];
+  #pragma unroll
+                for (int k = 0; k < UPT; ++k) {
+                  const int n = slb + S0 * k;
+                  zv[k] = zl[zbase[o] + (n < Kl ? n : 0)];
+                }
+                float acc = 0.0f;
+  #pragma unroll
+                for (int k = 0; k < UPT; ++k) {
+                  const int n = slb + S0 * k;
+                  acc += (n < Kl ? uv[o * UPT + k] : 0.0f) * zv[k];
+                }
+                acc = group_sum_rt(acc, S0);
+                if (yslot[o] >= 0 && slb == 0) ys[yslot[o]] = acc + bs[yslot[o]];
+              }
+            } else {
+              // S is a power of two (1 .. 16)
+              const int S = __builtin_amdgcn_readlane(vlanes, l), lgS = 31 - __builtin_clz(S);
+              const int OPP = kThreads >> lgS, os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
+              for (int base = 0; base < outs; base += OPP) {
+                const int ol = base + os;
+                float acc = 0.0f;
+                int q = 0, rr = 0;
+                if (ol < outs) {
+                  q = ol / rc;
+                  rr = ol - q * rc;
+                  const float* zg = zl + ((G == 4) ? q : 0) * Kmax;
+                  if (a.ustride) {
+                    const float* urow = us + (size_t)(q * RP + rr) * a.ustride;
+  #pragma unroll 8
+                    for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+                  } else {
+                    const float* urow = a.Ut + (size_t)(q * H + r0 + rr) * N;
+  #pragma unroll 8
+                    for (int n = sl; n < Kl; n += S) acc += urow[n] * zg[n];
+                  }
+                }
+                acc = group_sum_rt(acc, S);
+                if (sl == 0 && ol < outs) ys[q * RP + rr] = acc + bs[q * RP + rr];
+              }
+            }
+            lds_barrier();
+            for (int rr = threadIdx.x; rr < rc; rr += kThreads) {
+              float c = cs[lb * RP + rr], hv2;
+              cell_update(ys[0 * RP + rr], ys[1 * RP + rr], ys[2 * RP + rr], ys[3 * RP + rr], c, hv2);
+              cs[lb * RP + rr] = c;
+              hown[lb * RP + rr] = hv2;
+              if (local) hs[lb * H + r0 + rr] = hv2;
+            }
+            lds_barrier();
           }
-          lds_barrier();
+
         }
       }
     }
@@ -692,7 +828,10 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
 // chunk are adjacent.  The term's entries are read once from HBM.  The
 // chunks are dealt over gridDim.y workgroups per term group, so that few
 // terms with long sequences (or wide x, hence small chunks) still fill the
-// device.
+// device.  XC is the widest chunk: xchunk == XC with 16-byte x rows takes
+// the vector path (xrow a multiple of 4), anything else the scalar one.  The
+// per-(t, b) sums run in the same order at every XC.
+template <int XC>
 __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xchunk, int xrow) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   float* xt = reinterpret_cast<float*>(lds_raw);
@@ -730,17 +869,16 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
   for (int cb = blockIdx.y * xchunk; cb < TB; cb += gridDim.y * xchunk) {
     const int cnt = min(xchunk, TB - cb);
     __syncthreads();
-    if (a.xvec && xchunk == kMaxXChunk) {
-      // lane (c, k4) loads x[cb+c][4k4 .. 4k4+3]; a wave's 64 writes of one
-      // component land in 64 distinct banks (row stride 20 = 16 + 4)
-      const int n = kMaxXChunk * (D >> 2);
+    if (a.xvec && xchunk == XC) {
+      // lane (c, k4) loads x[cb+c][4k4 .. 4k4+3] and writes it down column c
+      const int n = XC * (D >> 2);
       constexpr int kStage = 8;                            // float4 loads in flight per thread
       for (int base = 0; base < n; base += kThreads * kStage) {
         float4 v[kStage];
 #pragma unroll
         for (int u = 0; u < kStage; ++u) {
           const int i = base + u * kThreads + (int)threadIdx.x;
-          const int c = i & (kMaxXChunk - 1), k4 = i >> 4;
+          const int c = i % XC, k4 = i / XC;
           v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
           if (i < n && c < cnt) v[u] = reinterpret_cast<const float4*>(a.x + (size_t)(cb + c) * D)[k4];
         }
@@ -748,7 +886,7 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
         for (int u = 0; u < kStage; ++u) {
           const int i = base + u * kThreads + (int)threadIdx.x;
           if (i < n) {
-            const int c = i & (kMaxXChunk - 1), k4 = i >> 4;
+            const int c = i % XC, k4 = i / XC;
             float* d = xt + (4 * k4) * xrow + c;
             d[0] = v[u].x;
             d[xrow] = v[u].y;
@@ -769,17 +907,17 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
       if (tau >= a.GK) break;
       const uint16_t* vi = a.vidx + (size_t)tau * NZ;
       const float* vv = a.vval + (size_t)tau * NZ;
-      float acc[kMaxXChunk];
+      float acc[XC];
 #pragma unroll
-      for (int c = 0; c < kMaxXChunk; ++c) acc[c] = 0.0f;
-      if (xchunk == kMaxXChunk) {
+      for (int c = 0; c < XC; ++c) acc[c] = 0.0f;
+      if ((xrow & 3) == 0 && xchunk == XC) {
 #pragma unroll
         for (int q = 0; q < kProjEntries; ++q) {
           if (64 * q < ne[w]) {
             const float v = ev[w][q];
             const float4* xk = reinterpret_cast<const float4*>(xt + ek[w][q] * xrow);
 #pragma unroll
-            for (int r = 0; r < kMaxXChunk / 4; ++r) {
+            for (int r = 0; r < XC / 4; ++r) {
               const float4 x4 = xk[r];
               acc[4 * r + 0] += v * x4.x;
               acc[4 * r + 1] += v * x4.y;
@@ -792,7 +930,7 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
           const float v = vv[e];
           const float4* xk = reinterpret_cast<const float4*>(xt + (int)vi[e] * xrow);
 #pragma unroll
-          for (int r = 0; r < kMaxXChunk / 4; ++r) {
+          for (int r = 0; r < XC / 4; ++r) {
             const float4 x4 = xk[r];
             acc[4 * r + 0] += v * x4.x;
             acc[4 * r + 1] += v * x4.y;
@@ -807,7 +945,7 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
             const float v = ev[w][q];
             const float* xk = xt + ek[w][q] * xrow;
 #pragma unroll
-            for (int c = 0; c < kMaxXChunk; ++c)
+            for (int c = 0; c < XC; ++c)
               if (c < xchunk) acc[c] += v * xk[c];
           }
         }
@@ -815,12 +953,12 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
           const float v = vv[e];
           const float* xk = xt + (int)vi[e] * xrow;
 #pragma unroll
-          for (int c = 0; c < kMaxXChunk; ++c)
+          for (int c = 0; c < XC; ++c)
             if (c < xchunk) acc[c] += v * xk[c];
         }
       }
 #pragma unroll
-      for (int c = 0; c < kMaxXChunk; ++c) {
+      for (int c = 0; c < XC; ++c) {
         if (c < cnt) {
           const float s = wave_sum(acc[c]);
           if (lane == 0) a.px[(size_t)tau * TB + cb + c] = s;
@@ -906,15 +1044,31 @@ size_t plan_progressive(RunArgs& a, int P) {
     a.ustride = smax * ((((Kmax + smax - 1) / smax)) | 1);
     if (layout_of(a, a.online).total > kLdsCap) a.ustride = 0;
   }
+  // one level over several sequences with U read from memory: phase B reads
+  // each U entry once per timestep for every sequence, K in the largest tile
+  // (a multiple of 16 lanes, at most 1024 terms) whose z of every pair fit
+  a.ktile = 0;
+  if (a.upt == 0 && a.ustride == 0 && !a.allpairs && a.L == 1 && a.B > 1 && a.B <= kTilePairs && P > 1 &&
+      Kmax > 0 && 4 * a.rows_per <= kThreads / a.lanes_b[0]) {
+    // at most kTileEntries U entries per lane and row in a tile, and at
+    // most kTileWords z words per gathering thread (448 of them)
+    int ktmax = std::min(kTileEntries * a.lanes_b[0], (Kmax + 15) / 16 * 16);
+    while (ktmax > 16 && a.G * ktmax > kTileWords * ((kThreads - 64) / a.B)) ktmax = ktmax / 32 * 16;
+    for (int kt = ktmax; kt >= 16; kt = kt / 32 * 16) {
+      a.ktile = kt;
+      if (layout_of(a, a.online).total <= kLdsCap) break;
+      a.ktile = 0;
+    }
+  }
   a.px_all = 1;
   if (layout_of(a, a.online).total > kLdsCap) a.px_all = 0;
   return layout_of(a, a.online).total;
 }
 
-template <int HPL, int OPT, int UPT, bool ONLINE, bool AP>
+template <int HPL, int OPT, int UPT, bool ONLINE, bool AP, bool TILE = false>
 hipError_t launch_kernel(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
   static bool attr_set = false;
-  const void* fn = (const void*)progressive_lstm_kernel<HPL, OPT, UPT, ONLINE, AP>;
+  const void* fn = (const void*)progressive_lstm_kernel<HPL, OPT, UPT, ONLINE, AP, TILE>;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsCap);
     if (e != hipSuccess) return e;
@@ -925,15 +1079,18 @@ hipError_t launch_kernel(const RunArgs& a, int blocks, int cooperative, size_t l
     void* args[] = {&copy};
     return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(kThreads), args, (unsigned)lds, stream);
   }
-  progressive_lstm_kernel<HPL, OPT, UPT, ONLINE, AP><<<dim3(blocks), dim3(kThreads), lds, stream>>>(a);
+  progressive_lstm_kernel<HPL, OPT, UPT, ONLINE, AP, TILE><<<dim3(blocks), dim3(kThreads), lds, stream>>>(a);
   return hipGetLastError();
 }
 
-// The all-pairs phase B is compiled only into the instances that launches
-// with several (level, sequence) pairs use: it costs the others registers.
+// The all-pairs and the K-tiled phase B are compiled only into the
+// instances that launches with several (level, sequence) pairs use: they
+// cost the others registers.
 template <int HPL, int OPT, int UPT, bool ONLINE = false>
 hipError_t launch_one(const RunArgs& a, int blocks, int cooperative, size_t lds, hipStream_t stream) {
   if (a.allpairs) return launch_kernel<HPL, OPT, UPT, ONLINE, true>(a, blocks, cooperative, lds, stream);
+  if constexpr (UPT == 0)
+    if (a.ktile > 0) return launch_kernel<HPL, OPT, UPT, ONLINE, false, true>(a, blocks, cooperative, lds, stream);
   return launch_kernel<HPL, OPT, UPT, ONLINE, false>(a, blocks, cooperative, lds, stream);
 }
 
@@ -956,34 +1113,44 @@ hipError_t launch_u(const RunArgs& a, int blocks, int cooperative, size_t lds, h
   return launch_one<HPL, 1, 0>(a, blocks, cooperative, lds, stream);
 }
 
-hipError_t launch_input_proj(const RunArgs& a, hipStream_t stream) {
-  if (a.GK > 0) {
-    // largest chunk of (t, b) pairs whose transposed x fits in LDS (odd row
-    // stride: the lanes' rows fall in different banks)
-    const int TB = a.T * a.B;
-    // full chunks of 16 (t, b) pairs use a 16-byte aligned row of 20 floats;
-    // smaller ones an odd row (the lanes' rows then fall in different banks)
-    int xchunk = kMaxXChunk, xrow = kMaxXChunk + 4;
-    if ((size_t)a.D * xrow * 4 > kLdsCap) {
-      xchunk = kMaxXChunk - 1;
-      while (xchunk > 1 && (size_t)a.D * (xchunk | 1) * 4 > kLdsCap) --xchunk;
-      xrow = xchunk | 1;
-    }
-    const size_t plds = (size_t)a.D * xrow * 4;
-    static bool proj_attr = false;
-    if (!proj_attr) {
-      hipError_t e = hipFuncSetAttribute((const void*)input_proj_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         (int)kLdsCap);
-      if (e != hipSuccess) return e;
-      proj_attr = true;
-    }
-    const int per_block = kWaves;       // one term per wave
-    const int gx = (a.GK + per_block - 1) / per_block;
-    const int gy = column_slices(gx, (TB + xchunk - 1) / xchunk);
-    input_proj_kernel<<<dim3(gx, gy), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
-    return hipGetLastError();
+template <int XC>
+hipError_t launch_input_proj_xc(const RunArgs& a, int gx, int gy, int xchunk, int xrow, size_t plds,
+                                hipStream_t stream) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)input_proj_kernel<XC>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsCap);
+    if (e != hipSuccess) return e;
+    attr_set = true;
   }
-  return hipSuccess;
+  input_proj_kernel<XC><<<dim3(gx, gy), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
+  return hipGetLastError();
+}
+
+hipError_t launch_input_proj(const RunArgs& a, hipStream_t stream) {
+  if (a.GK <= 0) return hipSuccess;
+  const int TB = a.T * a.B;
+  const int gx = (a.GK + kWaves - 1) / kWaves;   // one term per wave
+  // few terms over a short sequence: chunks of 4 (t, b) pairs, each its own
+  // workgroup, so that the staging latency is spread over more workgroups
+  // (driving shape, T = 16, up to 512 terms: 6 us against 11 with one
+  // workgroup per term group); otherwise chunks of 16
+  const int c4 = (TB + 3) / 4;
+  if ((size_t)a.D * 4 * 4 <= kLdsCap && (long long)gx * c4 <= (long long)std::max(1, a.num_cu))
+    return launch_input_proj_xc<4>(a, gx, c4, 4, 4, (size_t)a.D * 4 * 4, stream);
+  // full chunks of 16 (t, b) pairs use a 16-byte aligned row of 20 floats
+  // (a wave's 64 writes of one component land in distinct banks); x too
+  // wide for that takes the largest smaller chunk that fits, with an odd row
+  // (the lanes' rows then fall in different banks)
+  int xchunk = kMaxXChunk, xrow = kMaxXChunk + 4;
+  if ((size_t)a.D * xrow * 4 > kLdsCap) {
+    xchunk = kMaxXChunk - 1;
+    while (xchunk > 1 && (size_t)a.D * (xchunk | 1) * 4 > kLdsCap) --xchunk;
+    xrow = xchunk | 1;
+  }
+  const size_t plds = (size_t)a.D * xrow * 4;
+  const int gy = column_slices(gx, (TB + xchunk - 1) / xchunk);
+  return launch_input_proj_xc<kMaxXChunk>(a, gx, gy, xchunk, xrow, plds, stream);
 }
 
 hipError_t launch_progressive(const RunArgs& a, int blocks, int cooperative, hipStream_t stream) {

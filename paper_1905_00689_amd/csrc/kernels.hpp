@@ -7,6 +7,9 @@
 namespace alstm {
 
 constexpr int kMaxLevels = 16;
+constexpr int kTilePairs = 8;           // sequences of a K-tiled phase B (RunArgs::ktile)
+constexpr int kTileEntries = 16;        // U entries per lane and row in one tile of it
+constexpr int kTileWords = 16;          // z words per gathering thread in one tile of it
 constexpr int kMaxOptions = 24;        // candidate budgets of an online (anytime) run
 constexpr int kThreads = 512;          // 8 wave64 per workgroup
 constexpr int kMaxXChunk = 16;         // (t, b) pairs accumulated per pass of the input projection
@@ -67,8 +70,12 @@ struct RunArgs {
   int bulk_h;      // 1: h exchanged in bulk (hbx + hflag), 0: as tagged words (hx)
   int allpairs;    // 1: phase B takes every (level, sequence) pair in one pass (z of all
                    //    pairs resident in LDS); 0: one pass per pair
+  int ktile;       // > 0 (one level, U read from memory): phase B reads each U entry
+                   //    once per timestep for every sequence, K in tiles of ktile
+                   //    terms whose z of every pair sit in LDS
   int hb_stride;   // words per step parity of hx and hbx: L*B*H (+1 online) rounded up to 4
   int P;           // workgroups of the launch
+  int num_cu;      // compute units of the device (sizes the input projection's grid)
   int lanes_a;     // lanes per term in phase A (16)
   unsigned tag_base;
   int levels[kMaxLevels];
@@ -244,6 +251,7 @@ struct BatchedArgs {
 
 // Sequences per cohort of the persistent batched recurrence (the MFMA tile width).
 constexpr int kCohort = 16;
+
 
 // Shape of a persistent batched launch at budget K: W workgroups per cohort
 // (32 hidden units each), `slots` cohorts in flight.  Returns 0 when the

@@ -132,8 +132,10 @@ DEADLINE = dict(D=2048, H=2048, T=64, B=8, index=5, xkind="relu", name="deadline
 PAPER = dict(D=8256, H=64, T=100, B=1, index=6, xkind="relu", wkind="decay", name="paper")
 # The driving shape with decaying-spectrum weights.
 DRIVING_DECAY = dict(D=2048, H=512, T=16, B=1, index=7, xkind="relu", wkind="decay", name="driving-decay")
+# The deadline shape with decaying-spectrum weights.
+DEADLINE_DECAY = dict(D=2048, H=2048, T=64, B=8, index=8, xkind="relu", wkind="decay", name="deadline-decay")
 
-NAMED = {w["name"]: w for w in (TINY, DRIVING, BATCHED, STACK, DEADLINE, PAPER, DRIVING_DECAY)}
+NAMED = {w["name"]: w for w in (TINY, DRIVING, BATCHED, STACK, DEADLINE, PAPER, DRIVING_DECAY, DEADLINE_DECAY)}
 
 
 def named(name, **override):
