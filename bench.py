@@ -807,7 +807,8 @@ def blas_info():
 
 
 TRAFFIC_PROFILES = {
-    "driving": ("driving_K512_p75_hbm_counters.md", ("kernels.hip", "kernels.hpp", "device_common.hpp")),
+    "driving": ("driving_K512_p75_hbm_counters.md",
+                ("kernels.hip", "kernels_pair.hip", "kernels.hpp", "device_common.hpp")),
     "batched": ("batched_K512_p75_hbm_counters.md", ("batched.hip", "kernels.hpp", "device_common.hpp")),
 }
 
