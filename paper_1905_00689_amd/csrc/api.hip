@@ -598,7 +598,8 @@ approx_lstm_status run_progressive(approx_lstm_model* m, const float* x, int32_t
   a.hb_stride = (int)round_up(LB * m->H + kword, 4);
   a.bulk_h = alstm::use_bulk_h(n_levels, B, m->H);
   const size_t px_floats = std::max<size_t>(1, (size_t)a.GK * T * B);
-  const size_t zx_words = std::max<size_t>(1, LB * P * a.owned_max);
+  // z words, then (K-tiled phase B) the y words of every pair's gate rows
+  const size_t zx_words = std::max<size_t>(1, LB * P * a.owned_max + (a.ktile > 0 ? LB * 4 * (size_t)m->H : 0));
   const size_t hx_words = 2 * (size_t)a.hb_stride;
   unsigned tag_seq = 0;
   size_t exch_off = 0;

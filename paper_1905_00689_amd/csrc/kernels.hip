@@ -167,28 +167,31 @@ __device__ void gather_every_pair(float* zs, const uint16_t* slot_term, const un
   }
 }
 
-// z gather of one tile of terms, [G*k0, G*(k0+kn)), for every (level,
-// sequence) pair of a one-level launch.  The K-tiled launch publishes z in
-// term order (word tau of the pair's block of P*OM words), so a tile's words
-// are contiguous.  The nthr gathering threads split into LB groups of
-// tpp = nthr / LB, one per pair; thread t of pair lb's group takes the
-// tile's terms G*k0 + t + tpp*k (k < NS), whose z land at
-// zt[(lb*G + tau % G)*KT + tau / G - k0].  Every load is issued at once and
+// z gather of one tile of one group's terms, n in [k0, k0 + kn) of group g,
+// for every (level, sequence) pair of a one-level launch.  The K-tiled
+// launch publishes z group-major (word g*Kmax + n of the pair's block of
+// P*OM words), so a tile's words are contiguous from goff = g*Kmax + k0.
+// The nthr gathering threads split into LB groups of tpp = nthr / LB, one
+// per pair; thread t of pair lb's group takes words r = t + tpp*k (k < NS),
+// whose z land at zt[lb*zpl + (r % S)*zrow + r / S]: phase-B lane sl's
+// terms k0 + sl + S*e, e ascending, are consecutive (zrow = KT/S + 4, a
+// multiple of 4 that spreads the lanes' 16-byte reads over the banks;
+// zpl = S * zrow).  Every load is issued at once and
 // only the words still missing are loaded again (after the first tile every
 // word has usually arrived: one load round trip per tile).  Bounded like
 // gather_level.
 template <int NS>
-__device__ void gather_tile(float* zt, const unsigned long long* src, int P, int OM, int LB, int G, int k0, int kn,
-                            int KT, unsigned tag, unsigned* err, int tid, int nthr) {
+__device__ void gather_tile(float* zt, const unsigned long long* src, size_t pstride, int LB, int goff, int kn, int lgS,
+                            int zrow, unsigned tag, unsigned* err, int tid, int nthr) {
   const int tpp = nthr / LB, lb = tid / tpp, t = tid - lb * tpp;
   if (lb >= LB) return;
-  const int per = G * kn;
-  const unsigned long long* sp = src + (size_t)lb * P * OM + G * k0 + t;
-  float* zl = zt + (size_t)lb * G * KT;
+  const unsigned long long* sp = src + (size_t)lb * pstride + goff + t;
+  float* zl = zt + (size_t)lb * (zrow << lgS);
+  const int sm = (1 << lgS) - 1;
   unsigned pending = 0;
 #pragma unroll
   for (int k = 0; k < NS; ++k)
-    if (t + tpp * k < per) pending |= 1u << k;
+    if (t + tpp * k < kn) pending |= 1u << k;
   unsigned spins = 0;
   while (pending) {
     unsigned long long w[NS];
@@ -198,9 +201,8 @@ __device__ void gather_tile(float* zt, const unsigned long long* src, int P, int
 #pragma unroll
     for (int k = 0; k < NS; ++k)
       if (((pending >> k) & 1u) && (unsigned)(w[k] >> 32) == tag) {
-        const int r = t + tpp * k;   // term G*k0 + r: group r % G, index k0 + r / G
-        const int g = G == 4 ? (r & 3) : r % G, nl = G == 4 ? (r >> 2) : r / G;
-        zl[g * KT + nl] = __uint_as_float((unsigned)w[k]);
+        const int r = t + tpp * k;
+        zl[(r & sm) * zrow + (r >> lgS)] = __uint_as_float((unsigned)w[k]);
         pending &= ~(1u << k);
       }
     if (pending && (++spins & 255u) == 0u &&
@@ -210,7 +212,7 @@ __device__ void gather_tile(float* zt, const unsigned long long* src, int P, int
       for (int k = 0; k < NS; ++k)
         if ((pending >> k) & 1u) {
           const int r = t + tpp * k;
-          zl[(r % G) * KT + r / G] = 0.0f;
+          zl[(r & sm) * zrow + (r >> lgS)] = 0.0f;
         }
       break;
     }
@@ -219,14 +221,14 @@ __device__ void gather_tile(float* zt, const unsigned long long* src, int P, int
 
 // words per thread: the planner keeps a tile within kTileWords words per
 // thread of a pair's group
-__device__ __forceinline__ void gather_tile_any(float* zt, const unsigned long long* src, int P, int OM, int LB, int G,
-                                                int k0, int kn, int KT, unsigned tag, unsigned* err, int tid,
-                                                int nthr) {
+__device__ __forceinline__ void gather_tile_any(float* zt, const unsigned long long* src, size_t pstride, int LB,
+                                                int goff, int kn, int lgS, int zrow, unsigned tag, unsigned* err,
+                                                int tid, int nthr) {
   const int tpp = nthr / LB;
-  const int per = (G * kn + tpp - 1) / tpp;
-  if (per <= 4) gather_tile<4>(zt, src, P, OM, LB, G, k0, kn, KT, tag, err, tid, nthr);
-  else if (per <= 8) gather_tile<8>(zt, src, P, OM, LB, G, k0, kn, KT, tag, err, tid, nthr);
-  else gather_tile<kTileWords>(zt, src, P, OM, LB, G, k0, kn, KT, tag, err, tid, nthr);
+  const int per = (kn + tpp - 1) / tpp;
+  if (per <= 4) gather_tile<4>(zt, src, pstride, LB, goff, kn, lgS, zrow, tag, err, tid, nthr);
+  else if (per <= 8) gather_tile<8>(zt, src, pstride, LB, goff, kn, lgS, zrow, tag, err, tid, nthr);
+  else gather_tile<kTileWords>(zt, src, pstride, LB, goff, kn, lgS, zrow, tag, err, tid, nthr);
 }
 
 // LDS carve-up shared by the host planner and the kernel (byte offsets).
@@ -244,7 +246,7 @@ __host__ __device__ inline Layout layout_of(const RunArgs& a, int online) {
   // z of one (level, seq), [g][Kmax]; a single workgroup keeps every pair's
   // (a K-tiled phase B holds one tile of every pair's z instead)
   const size_t zfl = ((a.P == 1 || a.allpairs) ? LB : 1) * (a.GK > 1 ? (size_t)a.GK : 1);
-  const size_t ztl = a.ktile > 0 ? LB * a.G * (size_t)a.ktile : 0;
+  const size_t ztl = a.ktile > 0 ? LB * (size_t)(a.ktile + 4 * a.lanes_b[0]) : 0;   // [pair][S][KT/S + 4]
   l.zs = o;     o = align16(o + 4 * (zfl > ztl ? zfl : ztl));
   // h_{t-1} per (level, seq); an online run receives K_t in one more slot
   l.hs = o;     o = align16(o + 4 * (LB * a.H + (online ? 1 : 0)));
@@ -501,10 +503,14 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
       for (int lb = 0; lb < LB; ++lb) {
         const int GKl = G * (ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, lb / B));
         const int nl = (GKl > j) ? (GKl - j + P - 1) / P : 0;
-        for (int i = lane; i < nl; i += 64)
-          // slot j*OM + i, or (K-tiled phase B) word tau = j + i*P: a tile's
-          // terms are then contiguous words
-          publish(a.zx + (size_t)lb * P * OM + (a.ktile > 0 ? j + i * P : j * OM + i), zown[lb * OM + i], tag);
+        for (int i = lane; i < nl; i += 64) {
+          // slot j*OM + i, or (K-tiled phase B) word g*Kmax + n of term
+          // tau = j + i*P = n*G + g: a tile's terms of one group are then
+          // contiguous words
+          const int tau = j + i * P;
+          const size_t wd = TILE ? (size_t)(tau & 3) * Kmax + (tau >> 2) : (size_t)(j * OM + i);   // TILE: G = 4
+          publish(a.zx + (size_t)lb * P * OM + wd, zown[lb * OM + i], tag);
+        }
       }
     }
 
@@ -611,24 +617,34 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
       } else {
         if constexpr (TILE) {
           {
-            // One level over several sequences, U read from memory: each
+            // One level over several sequences, U read from memory, G = 4,
+            // P a multiple of 4.  Workgroup j keeps the cell update of its
+            // units [r0, r0 + rc) but accumulates the rows of gate gq = j % 4
+            // for the 4*RP units of its block (workgroups 4*(j/4) .. +3,
+            // whose cell units those are): it needs only group gq's z.  Each
             // lane reads each of its U entries once per timestep and applies
-            // it to every sequence (one accumulator per pair and row), K in
-            // tiles of KT terms whose z of every pair are gathered into LDS
-            // (zs[(lb*G + g)*KT + n - k0]).  Per pair the sums run in the
+            // it to every sequence (one accumulator per sequence), K in tiles
+            // of KT terms whose group-gq z of every sequence are gathered
+            // into LDS (zs[lb*KT + n - k0]).  y = sum + bias goes to the cell
+            // owners as tagged words (y words after the pairs' z blocks:
+            // [lb][gate][H]).  Per (row, sequence) the sums run in the
             // per-pair pass's order (entries sl, sl + S, ... ascending, then
             // the S-lane reduction, then the bias).
             const int KT = a.ktile;
             const int Kl = ONLINE ? kcur : __builtin_amdgcn_readlane(vlev, 0);
             const int S = __builtin_amdgcn_readlane(vlanes, 0), lgS = 31 - __builtin_clz(S);
             const int os = (int)threadIdx.x >> lgS, sl = (int)threadIdx.x & (S - 1);
-            // one output row per thread (the planner's condition)
+            const int gq = j & 3;
+            const int ub0 = (j >> 2) * 4 * RP;                 // first unit of the block
+            const int zrow = (KT >> lgS) + 4, zpl = zrow << lgS;   // LDS row of a lane, block of a pair
+            unsigned long long* yx = a.zx + (size_t)LB * P * OM;
+            // one output row per thread (the planner's condition): gate gq,
+            // unit ub0 + os
             float acc[kTilePairs];
-            const int ol = os;
-            const bool rv = ol < outs;
-            const int q = rv ? ol / rc : 0, rr0 = rv ? ol - q * rc : 0;
-            const float* urow = a.Ut + (size_t)(q * H + r0 + rr0) * N;
-            const int yq = q * RP + rr0, zq = ((G == 4) ? q : 0) * KT;
+            const int u = ub0 + os;
+            const bool rv = os < 4 * RP && u < H;
+            const float* urow = a.Ut + (size_t)(gq * H + (rv ? u : 0)) * N;
+            const float brow = rv ? a.bias[gq * H + u] : 0.0f;
 #pragma unroll
             for (int lb = 0; lb < kTilePairs; ++lb) acc[lb] = 0.0f;
             for (int k0 = 0; k0 < Kl; k0 += KT) {
@@ -642,18 +658,25 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
               }
               if (k0 > 0) lds_barrier();   // every read of the previous tile is done
               if (!publisher)
-                gather_tile_any(zs, a.zx, P, OM, LB, G, k0, kn, KT, tag, a.err, threadIdx.x, gthr);
+                gather_tile_any(zs, a.zx, (size_t)P * OM, LB, gq * Kmax + k0, kn, lgS, zrow, tag, a.err,
+                                threadIdx.x, gthr);
               lds_barrier();
               if (stamp && k0 == 0) a.stamps[4 + 4 * t] = clock64();
               if (rv) {
-                const float* zg = zs + zq - k0;
+                // lane sl's z of the tile: zs[lb*zpl + sl*zrow + e], e ascending
+                const float* zl = zs + sl * zrow;
 #pragma unroll
-                for (int e = 0; e < kTileEntries; ++e) {
-                  const int n = k0 + sl + S * e;
-                  if (n < k0 + kn) {
+                for (int e4 = 0; e4 < kTileEntries / 4; ++e4) {
+                  if (4 * e4 >= (KT >> lgS)) break;   // the lane's row holds KT / S values
 #pragma unroll
-                    for (int lb = 0; lb < kTilePairs; ++lb)
-                      if (lb < LB) acc[lb] += ut[e] * zg[lb * G * KT + n];
+                  for (int lb = 0; lb < kTilePairs; ++lb) {
+                    if (lb >= LB) break;
+                    const float4 z4 = *reinterpret_cast<const float4*>(zl + lb * zpl + 4 * e4);
+                    const int e = 4 * e4;
+                    if (sl + S * e < kn) acc[lb] += ut[e] * z4.x;
+                    if (sl + S * (e + 1) < kn) acc[lb] += ut[e + 1] * z4.y;
+                    if (sl + S * (e + 2) < kn) acc[lb] += ut[e + 2] * z4.z;
+                    if (sl + S * (e + 3) < kn) acc[lb] += ut[e + 3] * z4.w;
                   }
                 }
               }
@@ -662,14 +685,35 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
             for (int lb = 0; lb < kTilePairs; ++lb)
               if (lb < LB) {
                 const float v = group_sum_rt(acc[lb], S);
-                if (sl == 0 && rv) ys[lb * 4 * RP + yq] = v + bs[yq];
+                if (sl == 0 && rv) publish(yx + ((size_t)lb * 4 + gq) * H + u, v + brow, tag);
               }
-            lds_barrier();
+            // the owned units' four gate rows from the block's workgroups
+            // (bounded polls), then the cell update
             for (int i = threadIdx.x; i < LB * rc; i += kThreads) {
               const int lb = i / rc, rr = i - lb * rc;
-              const float* yl = ys + lb * 4 * RP;
+              const unsigned long long* yw = yx + (size_t)lb * 4 * H + r0 + rr;
+              float yv[4] = {0.f, 0.f, 0.f, 0.f};
+              unsigned pending = 0xFu, spins = 0;
+              while (pending) {
+                unsigned long long w4[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                  if ((pending >> q) & 1u) w4[q] = load_tagged(yw + (size_t)q * H);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                  if (((pending >> q) & 1u) && (unsigned)(w4[q] >> 32) == tag) {
+                    yv[q] = __uint_as_float((unsigned)w4[q]);
+                    pending &= ~(1u << q);
+                  }
+                if (pending && (++spins & 255u) == 0u &&
+                    (spins >= kSpinLimit ||
+                     __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+                  __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                  pending = 0;
+                }
+              }
               float c = cs[lb * RP + rr], hv2;
-              cell_update(yl[0 * RP + rr], yl[1 * RP + rr], yl[2 * RP + rr], yl[3 * RP + rr], c, hv2);
+              cell_update(yv[0], yv[1], yv[2], yv[3], c, hv2);
               cs[lb * RP + rr] = c;
               hown[lb * RP + rr] = hv2;
             }
@@ -831,7 +875,9 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
 // device.  XC is the widest chunk: xchunk == XC with 16-byte x rows takes
 // the vector path (xrow a multiple of 4), anything else the scalar one.  The
 // per-(t, b) sums run in the same order at every XC.
-template <int XC>
+// PT terms per wave (consecutive terms of the workgroup's PT*8): with many
+// terms, several share each staged chunk of x.
+template <int XC, int PT>
 __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xchunk, int xrow) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   float* xt = reinterpret_cast<float*>(lds_raw);
@@ -840,7 +886,7 @@ __global__ void __launch_bounds__(kThreads) input_proj_kernel(RunArgs a, int xch
   // the wave's term's first 64*kProjEntries x-part entries sit in registers,
   // loaded (unconditionally, masked afterwards) before x is staged so that
   // their HBM latency overlaps the staging
-  constexpr int kProjTerms = 1, kProjEntries = 16;
+  constexpr int kProjTerms = PT, kProjEntries = 16 / PT;
   int ne[kProjTerms];
   float ev[kProjTerms][kProjEntries];
   int ek[kProjTerms][kProjEntries];
@@ -1048,13 +1094,15 @@ size_t plan_progressive(RunArgs& a, int P) {
   // each U entry once per timestep for every sequence, K in the largest tile
   // (a multiple of 16 lanes, at most 1024 terms) whose z of every pair fit
   a.ktile = 0;
-  if (a.upt == 0 && a.ustride == 0 && !a.allpairs && a.L == 1 && a.B > 1 && a.B <= kTilePairs && P > 1 &&
-      Kmax > 0 && 4 * a.rows_per <= kThreads / a.lanes_b[0]) {
+  if (a.upt == 0 && a.ustride == 0 && !a.allpairs && a.L == 1 && a.B > 1 && a.B <= kTilePairs && a.G == 4 &&
+      P > 1 && P % 4 == 0 && Kmax > 0 && 4 * a.rows_per <= kThreads / a.lanes_b[0]) {
     // at most kTileEntries U entries per lane and row in a tile, and at
     // most kTileWords z words per gathering thread (448 of them)
-    int ktmax = std::min(kTileEntries * a.lanes_b[0], (Kmax + 15) / 16 * 16);
-    while (ktmax > 16 && a.G * ktmax > kTileWords * ((kThreads - 64) / a.B)) ktmax = ktmax / 32 * 16;
-    for (int kt = ktmax; kt >= 16; kt = kt / 32 * 16) {
+    // (KT a multiple of 4 S: a lane's terms of a tile are read as 16-byte vectors)
+    const int s4 = 4 * a.lanes_b[0];
+    int ktmax = std::min(kTileEntries * a.lanes_b[0], (Kmax + s4 - 1) / s4 * s4);
+    while (ktmax > s4 && ktmax > kTileWords * ((kThreads - 64) / a.B)) ktmax = ktmax / (2 * s4) * s4;
+    for (int kt = ktmax; kt >= s4; kt = kt / (2 * s4) * s4) {
       a.ktile = kt;
       if (layout_of(a, a.online).total <= kLdsCap) break;
       a.ktile = 0;
@@ -1113,17 +1161,17 @@ hipError_t launch_u(const RunArgs& a, int blocks, int cooperative, size_t lds, h
   return launch_one<HPL, 1, 0>(a, blocks, cooperative, lds, stream);
 }
 
-template <int XC>
+template <int XC, int PT = 1>
 hipError_t launch_input_proj_xc(const RunArgs& a, int gx, int gy, int xchunk, int xrow, size_t plds,
                                 hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)input_proj_kernel<XC>,
+    hipError_t e = hipFuncSetAttribute((const void*)input_proj_kernel<XC, PT>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsCap);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  input_proj_kernel<XC><<<dim3(gx, gy), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
+  input_proj_kernel<XC, PT><<<dim3(gx, gy), dim3(kThreads), plds, stream>>>(a, xchunk, xrow);
   return hipGetLastError();
 }
 
@@ -1149,6 +1197,14 @@ hipError_t launch_input_proj(const RunArgs& a, hipStream_t stream) {
     xrow = xchunk | 1;
   }
   const size_t plds = (size_t)a.D * xrow * 4;
+  // terms enough for every compute unit at 4 terms per wave: each staged
+  // chunk of x then serves 32 terms instead of 8 (deadline shape, 8192
+  // terms over 32 chunks: the staging was 4 GB over the device)
+  if (gx >= 4 * std::max(1, a.num_cu)) {
+    const int gx4 = (a.GK + 4 * kWaves - 1) / (4 * kWaves);
+    const int gy4 = column_slices(gx4, (TB + xchunk - 1) / xchunk);
+    return launch_input_proj_xc<kMaxXChunk, 4>(a, gx4, gy4, xchunk, xrow, plds, stream);
+  }
   const int gy = column_slices(gx, (TB + xchunk - 1) / xchunk);
   return launch_input_proj_xc<kMaxXChunk>(a, gx, gy, xchunk, xrow, plds, stream);
 }

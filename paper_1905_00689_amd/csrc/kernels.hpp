@@ -70,9 +70,12 @@ struct RunArgs {
   int bulk_h;      // 1: h exchanged in bulk (hbx + hflag), 0: as tagged words (hx)
   int allpairs;    // 1: phase B takes every (level, sequence) pair in one pass (z of all
                    //    pairs resident in LDS); 0: one pass per pair
-  int ktile;       // > 0 (one level, U read from memory): phase B reads each U entry
-                   //    once per timestep for every sequence, K in tiles of ktile
-                   //    terms whose z of every pair sit in LDS
+  int ktile;       // > 0 (one level, U read from memory, G = 4, P % 4 == 0): phase B
+                   //    reads each U entry once per timestep for every sequence, K in
+                   //    tiles of ktile terms of one group whose z of every pair sit in
+                   //    LDS; workgroup j accumulates the gate j % 4 rows of its block of
+                   //    four workgroups' units, and y travels to the cell owners in
+                   //    LB * 4 * H tagged words after the LB * P * owned_max z words
   int hb_stride;   // words per step parity of hx and hbx: L*B*H (+1 online) rounded up to 4
   int P;           // workgroups of the launch
   int num_cu;      // compute units of the device (sizes the input projection's grid)
