@@ -111,9 +111,11 @@ void tri_solve_shifted(const double* a, const double* b, int m, double lam, doub
   }
 }
 
-// Largest eigenvalue of the m x m tridiagonal (a, b) by bisection on the
-// Sturm count, and its unit eigenvector s by inverse iteration.
-double tri_top_eigen(const double* a, const double* b, int m, std::vector<double>& s) {
+// Eigenpair idx (0: the largest, 1: the second largest, ...) of the m x m
+// symmetric tridiagonal matrix: Sturm-count bisection for the eigenvalue
+// (count(x) = eigenvalues below x; lambda_idx is the least x with
+// count(x) >= m - idx), then inverse iteration for the unit vector s.
+double tri_eigen_from_top(const double* a, const double* b, int m, int idx, std::vector<double>& s) {
   s.assign(m, 0.0);
   if (m == 1) {
     s[0] = 1.0;
@@ -129,14 +131,14 @@ double tri_top_eigen(const double* a, const double* b, int m, std::vector<double
   }
   const double eps = 2.220446049250313e-16;
   double pivmin = std::max(1e-290, 1e-290 * bmax2);
-  // invariant: count(lo) <= m-1 (lam_max >= lo), count(hi) == m (lam_max < hi)
+  // invariant: count(lo) < m-idx (lambda_idx >= lo), count(hi) >= m-idx (lambda_idx < hi)
   hi += eps * scale + 1e-300;
   lo -= eps * scale + 1e-300;
   for (int it = 0; it < 200; ++it) {
     double mid = 0.5 * (lo + hi);
     if (mid <= lo || mid >= hi) break;
     if (hi - lo <= 2.0 * eps * std::max(std::fabs(lo), std::fabs(hi))) break;
-    if (sturm_count(a, b, m, mid, pivmin) == m)
+    if (sturm_count(a, b, m, mid, pivmin) >= m - idx)
       hi = mid;
     else
       lo = mid;
@@ -158,10 +160,18 @@ double tri_top_eigen(const double* a, const double* b, int m, std::vector<double
   return lam;
 }
 
+double tri_top_eigen(const double* a, const double* b, int m, std::vector<double>& s) {
+  return tri_eigen_from_top(a, b, m, 0, s);
+}
+
 }  // namespace
 
 double tridiag_top(const double* a, const double* b, int m, std::vector<double>& s) {
   return tri_top_eigen(a, b, m, s);
+}
+
+double tridiag_second(const double* a, const double* b, int m, std::vector<double>& s) {
+  return tri_eigen_from_top(a, b, m, 1, s);
 }
 
 void lanczos_start(double* q, int n) {

@@ -49,7 +49,10 @@ void store_term(GroupFactors& out, int t, double s, std::vector<double>& uu, std
 // tridiag_top: largest eigenvalue and unit eigenvector s of the m x m
 // symmetric tridiagonal matrix with diagonal a and off-diagonal b.
 double tridiag_top(const double* a, const double* b, int m, std::vector<double>& s);
-// lanczos_start: the fixed unit start vector of every Lanczos solve.
+// tridiag_second: the second largest eigenvalue and a unit eigenvector.
+double tridiag_second(const double* a, const double* b, int m, std::vector<double>& s);
+// lanczos_start: the fixed unit start vector of every host Lanczos solve
+// (and of each group's first device solve).
 void lanczos_start(double* q, int n);
 
 // Factorise the G groups of W ([G*rows][cols] row-major, float64; group g is

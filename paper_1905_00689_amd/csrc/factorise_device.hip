@@ -10,7 +10,10 @@
 //   * the Gram matrix M M^T is kept up to date by the rank-2 change that the
 //     residual update makes, and recomputed exactly every few steps;
 //   * Lanczos with full reorthogonalisation (two classical Gram-Schmidt
-//     passes) runs on it from a fixed start, in blocks of 8 iterations
+//     passes) runs on it, the first solve of each group from the host
+//     factorisation's fixed start and each later one from the previous
+//     solve's top and second Ritz vectors plus that fixed vector (a warm
+//     start: fewer iterations to the same tolerance), in blocks of 8 iterations
 //     captured once as a HIP graph; the host reads the tridiagonal
 //     coefficients after each block (one block behind the device) and solves
 //     the small tridiagonal eigenproblem for the convergence test and the
@@ -325,14 +328,23 @@ __global__ void __launch_bounds__(kFT) residual_update_kernel(double* __restrict
   if (d != 0.0) M[g * sM + e] -= d;
 }
 
-// Q[0] = q0 and k = 0 for every group.
+// q0[g] += qf (the fixed start vector) for the flagged groups.
+__global__ void __launch_bounds__(kFT) add_start_kernel(double* __restrict__ q0, const double* __restrict__ qf, int n,
+                                                         const int* __restrict__ act) {
+  const int g = blockIdx.z;
+  if (!act[g]) return;
+  const int i = blockIdx.x * kFT + threadIdx.x;
+  if (i < n) q0[(size_t)g * n + i] += qf[i];
+}
+
+// Q[0] = q0 (the group's start vector, q0 + g*n) and k = 0 for every group.
 __global__ void __launch_bounds__(kFT) start_kernel(double* __restrict__ Q, const double* __restrict__ q0,
                                                      int* __restrict__ kk, int n, size_t sQ,
                                                      const int* __restrict__ act) {
   const int g = blockIdx.z;
   if (!act[g]) return;
   const int i = blockIdx.x * kFT + threadIdx.x;
-  if (i < n) Q[g * sQ + i] = q0[i];
+  if (i < n) Q[g * sQ + i] = q0[(size_t)g * n + i];
   if (blockIdx.x == 0 && threadIdx.x == 0) kk[g] = 0;
 }
 
@@ -405,8 +417,8 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
   FD_TRY(hipStreamCreateWithFlags(&res.stream, hipStreamNonBlocking), "hipStreamCreate");
   hipStream_t stream = res.stream;
   DevBuf& buf = res.buf;
-  double *dM, *dG, *dQ, *dw, *dc1, *dc2, *dal, *dbe, *dy, *dx, *dpart, *da, *db, *dw2, *dsb, *dq0, *dritz;
-  int *dact, *dcnt, *dk;
+  double *dM, *dG, *dQ, *dw, *dc1, *dc2, *dal, *dbe, *dy, *dx, *dpart, *da, *db, *dw2, *dsb, *dq0, *dqf, *dritz, *dritz2;
+  int *dact, *dact2, *dcnt, *dk;
   FD_TRY(buf.alloc(dM, G * sM), "hipMalloc(residual)");
   FD_TRY(buf.alloc(dG, G * sG), "hipMalloc(Gram)");
   FD_TRY(buf.alloc(dQ, G * sQ), "hipMalloc(Lanczos basis)");
@@ -423,7 +435,10 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
   FD_TRY(buf.alloc(db, (size_t)G * m), "hipMalloc");
   FD_TRY(buf.alloc(dw2, (size_t)G * n), "hipMalloc");
   FD_TRY(buf.alloc(dsb, (size_t)2 * G), "hipMalloc");
-  FD_TRY(buf.alloc(dq0, (size_t)n), "hipMalloc");
+  FD_TRY(buf.alloc(dq0, (size_t)G * n), "hipMalloc");
+  FD_TRY(buf.alloc(dqf, (size_t)n), "hipMalloc");
+  FD_TRY(buf.alloc(dritz2, G * sc), "hipMalloc");
+  FD_TRY(buf.alloc(dact2, (size_t)G), "hipMalloc");
   FD_TRY(buf.alloc(dact, (size_t)G), "hipMalloc");
   FD_TRY(buf.alloc(dcnt, (size_t)G), "hipMalloc");
   FD_TRY(buf.alloc(dk, (size_t)G), "hipMalloc");
@@ -443,9 +458,13 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
       }
       FD_TRY(hipMemcpy(dM + g * sM, hM.data(), sM * 8, hipMemcpyHostToDevice), "upload residual");
     }
+    // every group's first solve starts from the fixed vector of the host
+    // factorisation
     std::vector<double> q0(n);
     lanczos_start(q0.data(), n);
-    FD_TRY(hipMemcpy(dq0, q0.data(), (size_t)n * 8, hipMemcpyHostToDevice), "upload start vector");
+    for (int g = 0; g < G; ++g)
+      FD_TRY(hipMemcpy(dq0 + (size_t)g * n, q0.data(), (size_t)n * 8, hipMemcpyHostToDevice), "upload start vector");
+    FD_TRY(hipMemcpy(dqf, q0.data(), (size_t)n * 8, hipMemcpyHostToDevice), "upload start vector");
   }
 
   // kIterBlock Lanczos iterations as one graph: w = G q_k, two classical
@@ -487,9 +506,9 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
   FD_TRY(gram(), "gram_kernel");
 
   std::vector<double> tau(G, 0.0), hy((size_t)G * n), hx((size_t)G * m);
-  std::vector<double> ha((size_t)G * n), hb((size_t)G * m), hsb(2 * G), hritz(G * sc, 0.0);
-  std::vector<int> hcnt(G), idx(cols);
-  std::vector<double> uu(rows), vv(cols), s;
+  std::vector<double> ha((size_t)G * n), hb((size_t)G * m), hsb(2 * G), hritz(G * sc, 0.0), hritz2(G * sc, 0.0);
+  std::vector<int> hcnt(G), idx(cols), has2(G, 0);
+  std::vector<double> uu(rows), vv(cols), s, s2;
 
   for (int t = 0; t < rank; ++t) {
     if (std::none_of(live.begin(), live.end(), [](int v) { return v != 0; })) break;
@@ -536,6 +555,17 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
             mdone[g] = mm;
             conv[g] = (resid <= opt.lanczos_tol * std::fabs(theta)) || mm == n;
             std::copy(s.begin(), s.end(), hritz.begin() + g * sc);
+            // the group's next solve starts from y1 + y2 + q_fixed (top and
+            // second Ritz vectors of this solve, and the fixed start): the
+            // next top direction lies close to y2 when the residual update
+            // removed the top one, and close to y1 when pruning left much
+            // of it behind; the fixed vector keeps a component along every
+            // direction, so that the solve cannot settle on a lower pair
+            has2[g] = mm >= 2 ? 1 : 0;
+            if (has2[g]) {
+              tridiag_second(al, be, mm, s2);
+              for (int i = 0; i < mm; ++i) hritz2[g * sc + i] = s[i] + s2[i];
+            }
           }
           break;
         }
@@ -551,6 +581,16 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
     combine_kernel<<<dim3(cdiv(n, 64), 1, G), dim3(kFT), 0, stream>>>(dQ, dritz, dy, dcnt, 0, kmax, n, sQ, sc, n, 1,
                                                                       dact);
     normalise_kernel<<<dim3(1, 1, G), dim3(kFT), 0, stream>>>(dy, n, n, dact);
+    // the next start vectors (groups whose solve had a second Ritz vector;
+    // the others keep theirs); the host arrays are read back by the stream
+    // synchronisation below before they can change
+    for (int g = 0; g < G; ++g) has2[g] = has2[g] && live[g];
+    FD_TRY(hipMemcpyAsync(dritz2, hritz2.data(), G * sc * 8, hipMemcpyHostToDevice, stream), "upload Ritz 2");
+    FD_TRY(hipMemcpyAsync(dact2, has2.data(), G * sizeof(int), hipMemcpyHostToDevice, stream), "upload flags 2");
+    combine_kernel<<<dim3(cdiv(n, 64), 1, G), dim3(kFT), 0, stream>>>(dQ, dritz2, dq0, dcnt, 0, kmax, n, sQ, sc, n, 1,
+                                                                      dact2);
+    add_start_kernel<<<dim3(cdiv(n, kFT), 1, G), dim3(kFT), 0, stream>>>(dq0, dqf, n, dact2);
+    normalise_kernel<<<dim3(1, 1, G), dim3(kFT), 0, stream>>>(dq0, n, n, dact2);
     mty_partial_kernel<<<dim3(cdiv(m, kFT), nrb, G), dim3(kFT), 0, stream>>>(dM, dy, dpart, n, m, sM, n, sp, dact);
     mty_reduce_kernel<<<dim3(cdiv(m, kFT), 1, G), dim3(kFT), 0, stream>>>(dpart, dx, nrb, m, sp, m, dact);
     FD_TRY(hipGetLastError(), "Ritz vector");
