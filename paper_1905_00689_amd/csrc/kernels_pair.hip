@@ -432,6 +432,16 @@ int plan_pair(PairArgs& a, int num_cu, int want, size_t* lds) {
     for (int p = 2; p <= cap && !P; ++p)
       if (fits(p)) P = p;
     if (!P) return 0;
+    // below 64 terms per group that width leaves each workgroup hundreds of
+    // output rows, and phase B then takes longer than the wider exchange
+    // costs: at least 16 workgroups from 17 terms per group, 32 from 64
+    // (each keeping 16 rows or more).  MI355X, driving shape, us per
+    // timestep at P = 4 / 8 / 16 / 32 / 64: K = 32 5.70 / 5.12 / 4.80 / 4.84
+    // / 5.42; K = 64 6.28 / 5.19 / 4.81 / 4.71 / 4.92; K = 128 - / 5.70 /
+    // 4.94 / 4.79 / 4.91; K = 256 32 and 64 equal (5.28, 5.27), K = 512 best
+    // at its own 64; outputs bitwise equal at every width.
+    const int floor_p = std::min({a.K >= 64 ? 32 : (a.K > 16 ? 16 : 0), (4 * a.H) / 16, cap});
+    if (P < floor_p && fits(floor_p)) P = floor_p;
     fits(P);
   }
   // register buckets: h-part entries per lane, U entries per row and lane
