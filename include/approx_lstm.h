@@ -210,10 +210,12 @@ approx_lstm_status approx_lstm_run_deadline(approx_lstm_model* m, const float* x
  * the best estimate for the time available).  One launch runs the sequence
  * with room for every term of the model; at the end of timestep t workgroup
  * 0 reads the device's wall clock and picks, among the candidate budgets
- * K = 0, 1, 2, 4, ..., rank, the largest whose predicted step time still
- * lets timestep t+1 end by (t+2) * deadline_us_per_step after the recurrence
- * began (time saved by earlier steps is spent later, time lost is recovered
- * by cutting later steps); the choice reaches every workgroup with the h
+ * K = 0, 1, 2, 4, ..., rank, the largest whose predicted step time fits
+ * one deadline plus an even share, over the remaining steps, of the time
+ * banked by the end of timestep t (the rest of timestep t, its h exchange,
+ * taken as measured on the previous step); a deficit is recovered at once,
+ * so timestep t+1 still ends by (t+2) * deadline_us_per_step after the
+ * recurrence began.  The choice reaches every workgroup with the h
  * exchange, so all compute with the same K_{t+1}.  K_0 is the largest
  * candidate predicted to fit one deadline.
  *

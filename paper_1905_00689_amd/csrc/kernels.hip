@@ -430,7 +430,11 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
   // online run: the same thread of workgroup 0 keeps the clock and chooses;
   // K_0 is the choice for one budget, the same in every workgroup
   const bool chooser = ONLINE && j == 0 && (int)threadIdx.x == kThreads - 64;
-  unsigned long long t_begin = 0ull;
+  unsigned long long t_begin = 0ull, t_decide = 0ull;
+  // the part of a timestep after the chooser's decision (its h publication
+  // and exchange), measured on the previous timestep: step t+1 starts that
+  // long after the decision for it
+  long long t_rest = 0;
   int kcur = 0;
   if constexpr (ONLINE) {
     kcur = a.sched ? a.sched[0] : online_pick(a, (long long)a.budget);
@@ -802,8 +806,15 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     unsigned long long* hxt = a.hx + (size_t)(t & 1) * a.hb_stride;
     if (ONLINE && chooser && t + 1 < T) {
       // K_{t+1}: timestep t+1 must end by (t+2) * budget after the start
-      const long long used = (long long)(wall_clock64() - t_begin);
-      const int knext = a.sched ? a.sched[t + 1] : online_pick(a, (long long)(t + 2) * (long long)a.budget - used);
+      // time banked by the end of step t (negative: behind the schedule);
+      // a surplus is spread evenly over the remaining steps (even budgets
+      // rather than a large K after a K = 0), a deficit recovered at once,
+      // so step t+1 still ends by (t+2) * budget
+      t_decide = wall_clock64();
+      const long long used = (long long)(t_decide - t_begin);
+      const long long banked = (long long)(t + 1) * (long long)a.budget - used - t_rest;
+      const long long share = banked > 0 ? banked / (long long)(T - t - 1) : banked;
+      const int knext = a.sched ? a.sched[t + 1] : online_pick(a, (long long)a.budget + share);
       if (!a.sched) a.kt[t + 1] = knext;
       const float kbits = __int_as_float(knext);
       if (local) hs[LB * H] = kbits;
@@ -849,6 +860,7 @@ __global__ void __launch_bounds__(kThreads) progressive_lstm_kernel(RunArgs a) {
     }
     lds_barrier();
     if (ONLINE && t + 1 < T) kcur = __float_as_int(hs[LB * H]);
+    if (ONLINE && chooser && t + 1 < T) t_rest = (long long)(wall_clock64() - t_decide);
   }
   if (stamp) {
     a.stamps[2 + 4 * T] = clock64();
