@@ -212,6 +212,20 @@ def test_driving_small_budgets_take_one_workgroup(driving_full_p75):
     assert p["pair_kernel"] == 1 and p["blocks"] > 1, p
 
 
+def test_driving_pair_widths(driving_full_p75):
+    """One-pair launch widths at the driving shape on 256 compute units: at
+    least 16 workgroups from 17 terms per group and 32 from 64 (below that
+    the narrowest width leaves hundreds of rows per workgroup), 64 at the
+    timed K = 512, one workgroup up to 16 terms."""
+    want = {1: 1, 16: 1, 17: 16, 32: 16, 63: 16, 64: 32, 128: 32, 256: 32, 512: 64}
+    for K, P in want.items():
+        p = B.approx_lstm_plan(driving_full_p75, 16, 1, [K], num_cu=256)
+        assert p["pair_kernel"] == 1 and p["blocks"] == P, (K, p)
+    # a smaller device caps the floor
+    p = B.approx_lstm_plan(driving_full_p75, 16, 1, [64], num_cu=8)
+    assert p["blocks"] <= 8, p
+
+
 def test_driving_no_pruning_gives_the_svd(driving):
     """NZ = C: the chain is the SVD of each gate (P4), over all 512 steps."""
     m = prep(driving, 512, p=0.0)
