@@ -373,10 +373,12 @@ struct Resources {
   hipGraphExec_t exec = nullptr;
   hipEvent_t ev[2] = {nullptr, nullptr};
   double* coef = nullptr;   // pinned host: two slots of [alpha | beta] for every group
+  void* stage = nullptr;    // pinned host: the per-term uploads and reads (see factorise_groups_device)
   DevBuf buf;
   ~Resources() {
     if (stream) (void)hipStreamSynchronize(stream);
     if (coef) (void)hipHostFree(coef);
+    if (stage) (void)hipHostFree(stage);
     for (hipEvent_t e : ev)
       if (e) (void)hipEventDestroy(e);
     if (exec) (void)hipGraphExecDestroy(exec);
@@ -489,20 +491,39 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
     FD_TRY(hipGraphInstantiate(&res.exec, res.graph, nullptr, nullptr, 0), "hipGraphInstantiate");
   }
 
+  // Pinned staging for the per-term transfers, one region per purpose, so
+  // that the copies run asynchronously and no extra synchronisation is
+  // needed: every region is rewritten only on the next term, after a stream
+  // synchronisation that its previous copy precedes (the read of y and x,
+  // which follows the flag, Ritz and start-vector uploads of a term; the
+  // update uploads of a term come after it and before the next term's).
+  enum { kActStart, kActLive, kActUpd, kActNum };
+  const size_t st_doubles = 2 * (size_t)G * sc + 2 * (size_t)G * n + 2 * (size_t)G * m + 2 * (size_t)G;
+  const size_t st_ints = (size_t)(kActNum + 2) * G;
+  FD_TRY(hipHostMalloc(&res.stage, st_doubles * 8 + st_ints * 4, hipHostMallocDefault), "hipHostMalloc");
+  double* st_ritz = static_cast<double*>(res.stage);   // [G][sc]
+  double* st_ritz2 = st_ritz + (size_t)G * sc;          // [G][sc]
+  double* st_a = st_ritz2 + (size_t)G * sc;             // [G][n]
+  double* st_y = st_a + (size_t)G * n;                  // [G][n]
+  double* st_b = st_y + (size_t)G * n;                  // [G][m]
+  double* st_x = st_b + (size_t)G * m;                  // [G][m]
+  double* st_sb = st_x + (size_t)G * m;                 // [2G]
+  int* st_act = reinterpret_cast<int*>(st_sb + 2 * (size_t)G);   // [kActNum][G]
+  int* st_cnt = st_act + (size_t)kActNum * G;                      // [G]
+  int* st_has2 = st_cnt + G;                                       // [G]
+
   std::vector<int> live(G, 1);   // group still producing terms
-  std::vector<int> act(G, 1);
-  // group flags for the next kernels; the copy completes before the host
-  // array can change again
-  auto set_act = [&](const std::vector<int>& v) -> hipError_t {
-    act = v;
-    hipError_t e = hipMemcpyAsync(dact, act.data(), G * sizeof(int), hipMemcpyHostToDevice, stream);
-    return e == hipSuccess ? hipStreamSynchronize(stream) : e;
+  // group flags for the next kernels, from staging region `which`
+  auto set_act = [&](const std::vector<int>& v, int which) -> hipError_t {
+    int* dst = st_act + (size_t)which * G;
+    std::copy(v.begin(), v.end(), dst);
+    return hipMemcpyAsync(dact, dst, G * sizeof(int), hipMemcpyHostToDevice, stream);
   };
   auto gram = [&]() -> hipError_t {
     gram_kernel<<<dim3(cdiv(n, kGramTile), cdiv(n, kGramTile), G), dim3(kFT), 0, stream>>>(dM, dG, n, m, sM, sG);
     return hipGetLastError();
   };
-  FD_TRY(set_act(live), "upload flags");
+  FD_TRY(set_act(live, kActLive), "upload flags");
   FD_TRY(gram(), "gram_kernel");
 
   std::vector<double> tau(G, 0.0), hy((size_t)G * n), hx((size_t)G * m);
@@ -514,14 +535,14 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
     if (std::none_of(live.begin(), live.end(), [](int v) { return v != 0; })) break;
     if (t > 0 && opt.gram_refresh > 0 && t % opt.gram_refresh == 0) FD_TRY(gram(), "gram_kernel");
     // ---- Lanczos on every live group's Gram matrix.  Blocks of kIterBlock
-    // iterations run ahead of the host's convergence test by one block: block
-    // b + 1 is queued before the coefficients of block b are examined (a
-    // group that has converged keeps iterating until all have; its later
-    // basis vectors are not used).  The test runs at the end of each block
-    // (and where beta vanishes), on the tridiagonal matrix of that size.
+    // iterations run ahead of the host's convergence test by one block while
+    // a solve is far from converged (a group that has converged keeps
+    // iterating until all have; its later basis vectors are not used).  The
+    // test runs at the end of each block (and where beta vanishes), on the
+    // tridiagonal matrix of that size.
     std::vector<int> lz = live;           // groups still iterating
     std::vector<int> mdone(G, 0), conv(G, 0);
-    FD_TRY(set_act(lz), "upload flags");
+    FD_TRY(set_act(lz, kActStart), "upload flags");
     start_kernel<<<dim3(cdiv(n, kFT), 1, G), dim3(kFT), 0, stream>>>(dQ, dq0, dk, n, sQ, dact);
     FD_TRY(hipGetLastError(), "start_kernel");
     const int nblk = (kmax + kIterBlock - 1) / kIterBlock;
@@ -533,9 +554,26 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
       if (e == hipSuccess) e = hipEventRecord(res.ev[b & 1], stream);
       return e;
     };
+    // Block b + 1 is queued before block b is examined unless every group
+    // still iterating is expected to converge within block b (its relative
+    // Ritz residual after block b - 1 times the factor of its last block at
+    // or below the tolerance): then the host examines block b first and
+    // queues b + 1 only if it is needed, instead of running a block whose
+    // result is discarded.  Which iterations the solves stop at does not
+    // depend on this.
+    std::vector<double> rel(G, HUGE_VAL), rate(G, 1.0);
+    int queued = 0;
     FD_TRY(enqueue_block(0), "Lanczos block");
     for (int b = 0; b < nblk; ++b) {
-      if (b + 1 < nblk) FD_TRY(enqueue_block(b + 1), "Lanczos block");
+      if (b + 1 < nblk && queued < b + 1) {
+        bool ahead = false;
+        for (int g = 0; g < G; ++g)
+          if (lz[g] && !(rel[g] * rate[g] <= opt.lanczos_tol)) ahead = true;
+        if (ahead) {
+          FD_TRY(enqueue_block(b + 1), "Lanczos block");
+          queued = b + 1;
+        }
+      }
       FD_TRY(hipEventSynchronize(res.ev[b & 1]), "hipEventSynchronize");
       const double* slot = res.coef + (size_t)(b & 1) * 2 * G * sc;
       const int prev = b * kIterBlock, done_k = std::min(kmax, prev + kIterBlock);
@@ -550,6 +588,11 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
           if (!last && bt != 0.0) continue;
           const double theta = tridiag_top(al, be, mm, s);
           const double resid = bt * std::fabs(s[mm - 1]);
+          {  // the relative residual and its factor over the last block
+            const double r = theta != 0.0 ? resid / std::fabs(theta) : HUGE_VAL;
+            rate[g] = (rel[g] < HUGE_VAL && rel[g] > 0.0) ? r / rel[g] : 1.0;
+            rel[g] = r;
+          }
           if (resid <= opt.lanczos_tol * std::fabs(theta) || bt == 0.0 || mm == kmax) {
             lz[g] = 0;
             mdone[g] = mm;
@@ -572,12 +615,17 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
         any = any || lz[g];
       }
       if (!any) break;
+      if (b + 1 < nblk && queued < b + 1) {   // not queued ahead, and still needed
+        FD_TRY(enqueue_block(b + 1), "Lanczos block");
+        queued = b + 1;
+      }
     }
     // ---- Ritz vector y and x = M^T y
-    for (int g = 0; g < G; ++g) hcnt[g] = mdone[g];
-    FD_TRY(set_act(live), "upload flags");
-    FD_TRY(hipMemcpyAsync(dritz, hritz.data(), G * sc * 8, hipMemcpyHostToDevice, stream), "upload Ritz");
-    FD_TRY(hipMemcpyAsync(dcnt, hcnt.data(), G * sizeof(int), hipMemcpyHostToDevice, stream), "upload counts");
+    for (int g = 0; g < G; ++g) st_cnt[g] = mdone[g];
+    std::copy(hritz.begin(), hritz.end(), st_ritz);
+    FD_TRY(set_act(live, kActLive), "upload flags");
+    FD_TRY(hipMemcpyAsync(dritz, st_ritz, G * sc * 8, hipMemcpyHostToDevice, stream), "upload Ritz");
+    FD_TRY(hipMemcpyAsync(dcnt, st_cnt, G * sizeof(int), hipMemcpyHostToDevice, stream), "upload counts");
     combine_kernel<<<dim3(cdiv(n, 64), 1, G), dim3(kFT), 0, stream>>>(dQ, dritz, dy, dcnt, 0, kmax, n, sQ, sc, n, 1,
                                                                       dact);
     normalise_kernel<<<dim3(1, 1, G), dim3(kFT), 0, stream>>>(dy, n, n, dact);
@@ -585,8 +633,10 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
     // the others keep theirs); the host arrays are read back by the stream
     // synchronisation below before they can change
     for (int g = 0; g < G; ++g) has2[g] = has2[g] && live[g];
-    FD_TRY(hipMemcpyAsync(dritz2, hritz2.data(), G * sc * 8, hipMemcpyHostToDevice, stream), "upload Ritz 2");
-    FD_TRY(hipMemcpyAsync(dact2, has2.data(), G * sizeof(int), hipMemcpyHostToDevice, stream), "upload flags 2");
+    std::copy(hritz2.begin(), hritz2.end(), st_ritz2);
+    std::copy(has2.begin(), has2.end(), st_has2);
+    FD_TRY(hipMemcpyAsync(dritz2, st_ritz2, G * sc * 8, hipMemcpyHostToDevice, stream), "upload Ritz 2");
+    FD_TRY(hipMemcpyAsync(dact2, st_has2, G * sizeof(int), hipMemcpyHostToDevice, stream), "upload flags 2");
     combine_kernel<<<dim3(cdiv(n, 64), 1, G), dim3(kFT), 0, stream>>>(dQ, dritz2, dq0, dcnt, 0, kmax, n, sQ, sc, n, 1,
                                                                       dact2);
     add_start_kernel<<<dim3(cdiv(n, kFT), 1, G), dim3(kFT), 0, stream>>>(dq0, dqf, n, dact2);
@@ -594,9 +644,11 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
     mty_partial_kernel<<<dim3(cdiv(m, kFT), nrb, G), dim3(kFT), 0, stream>>>(dM, dy, dpart, n, m, sM, n, sp, dact);
     mty_reduce_kernel<<<dim3(cdiv(m, kFT), 1, G), dim3(kFT), 0, stream>>>(dpart, dx, nrb, m, sp, m, dact);
     FD_TRY(hipGetLastError(), "Ritz vector");
-    FD_TRY(hipMemcpyAsync(hy.data(), dy, (size_t)G * n * 8, hipMemcpyDeviceToHost, stream), "read y");
-    FD_TRY(hipMemcpyAsync(hx.data(), dx, (size_t)G * m * 8, hipMemcpyDeviceToHost, stream), "read x");
+    FD_TRY(hipMemcpyAsync(st_y, dy, (size_t)G * n * 8, hipMemcpyDeviceToHost, stream), "read y");
+    FD_TRY(hipMemcpyAsync(st_x, dx, (size_t)G * m * 8, hipMemcpyDeviceToHost, stream), "read x");
     FD_TRY(hipStreamSynchronize(stream), "hipStreamSynchronize");
+    std::copy(st_y, st_y + (size_t)G * n, hy.begin());
+    std::copy(st_x, st_x + (size_t)G * m, hx.begin());
     // ---- sigma, sign, mask (host), and the update operands
     std::vector<int> upd(G, 0);
     for (int g = 0; g < G; ++g) {
@@ -657,10 +709,13 @@ int factorise_groups_device(const double* W, int G, int rows, int cols, int rank
     }
     if (std::none_of(upd.begin(), upd.end(), [](int v) { return v != 0; })) continue;
     // ---- residual and Gram updates on the device
-    FD_TRY(set_act(upd), "upload flags");
-    FD_TRY(hipMemcpyAsync(da, ha.data(), (size_t)G * n * 8, hipMemcpyHostToDevice, stream), "upload a");
-    FD_TRY(hipMemcpyAsync(db, hb.data(), (size_t)G * m * 8, hipMemcpyHostToDevice, stream), "upload b");
-    FD_TRY(hipMemcpyAsync(dsb, hsb.data(), (size_t)2 * G * 8, hipMemcpyHostToDevice, stream), "upload scales");
+    std::copy(ha.begin(), ha.end(), st_a);
+    std::copy(hb.begin(), hb.end(), st_b);
+    std::copy(hsb.begin(), hsb.end(), st_sb);
+    FD_TRY(set_act(upd, kActUpd), "upload flags");
+    FD_TRY(hipMemcpyAsync(da, st_a, (size_t)G * n * 8, hipMemcpyHostToDevice, stream), "upload a");
+    FD_TRY(hipMemcpyAsync(db, st_b, (size_t)G * m * 8, hipMemcpyHostToDevice, stream), "upload b");
+    FD_TRY(hipMemcpyAsync(dsb, st_sb, (size_t)2 * G * 8, hipMemcpyHostToDevice, stream), "upload scales");
     rowdot_kernel<<<dim3(cdiv(n, kFW), 1, G), dim3(kFT), 0, stream>>>(dM, db, dw2, n, m, sM, m, n, dact);
     gram_update_kernel<<<dim3(cdiv((size_t)n * n, kFT), 1, G), dim3(kFT), 0, stream>>>(dG, da, dw2, dsb, n, sG, n,
                                                                                        dact);
