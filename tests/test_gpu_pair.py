@@ -53,7 +53,7 @@ def driving_p75():
     return w, prep(w, 512, 0.75)
 
 
-@pytest.mark.parametrize("K", [1, 2, 8, 16, 32, 64, 128, 256, 384, 512])
+@pytest.mark.parametrize("K", [1, 2, 8, 16, 17, 32, 63, 64, 128, 256, 384, 512])
 def test_pair_kernel_driving_every_shape(driving_p75, K):
     w, m = driving_p75
     say("driving p=0.75, one pair, K", K)
@@ -67,6 +67,15 @@ def test_pair_kernel_driving_launch_widths(driving_p75, blocks):
     w, m = driving_p75
     say("driving K=512 on", blocks, "workgroups")
     check(m, w, 512, blocks=blocks)
+
+
+@pytest.mark.parametrize("blocks", [4, 8, 16, 64])
+def test_pair_kernel_driving_small_budget_widths(driving_p75, blocks):
+    """K = 64 on 4 to 64 workgroups (the automatic width is 32): hundreds of
+    rows per workgroup down to eight, the same bits."""
+    w, m = driving_p75
+    say("driving K=64 on", blocks, "workgroups")
+    check(m, w, 64, blocks=blocks)
 
 
 def test_pair_kernel_initial_state_and_tiny_groupings():
