@@ -732,7 +732,8 @@ def bench_batched(args, torch, emit=True, step_dist=True):
                 "traffic": measured_traffic("batched") if (K == 512 and abs(args.prune - 0.75) < 1e-9) else None,
                 "kernel": "one step: batched_xproj_kernel + batched_persistent_kernel (T timesteps in one launch)",
                 "flops_per_launch": flops, "algorithmic_flops_per_launch": algo,
-                "algorithmic_tflops": round(algo / (ms * 1e-3) / 1e12, 2)}
+                "algorithmic_tflops": round(algo / (ms * 1e-3) / 1e12, 2),
+                "algorithmic_frac": round(algo / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
     cpu = None if args.no_cpu_baseline else cpu_baseline_batched(m, wl, K, args.cpu_seconds)
     out = {
         "metric": "LSTM timesteps/sec at refinement budget K (and us/timestep vs K)",
