@@ -143,15 +143,18 @@ struct approx_lstm_model {
   size_t phx_cap = 0;
   unsigned* d_pflag = nullptr;       // [2][slots][W]
   size_t pflag_cap = 0;
+  float* d_ppart = nullptr;          // partial x-projections of a split contraction
+  size_t ppart_cap = 0;              // floats
 
   ~approx_lstm_model() {
     if (!has_dev && !d_px && !d_zx && !d_hx && !d_hbx && !d_hflag && !d_err && !d_stamps && !d_stack && !d_bz &&
-        !d_bh && !d_bc && !d_kt && !d_pzx && !d_phx && !d_pflag)
+        !d_bh && !d_bc && !d_kt && !d_pzx && !d_phx && !d_pflag && !d_ppart)
       return;
     DeviceScope ds(device);
     dfree(d_pzx);
     dfree(d_phx);
     dfree(d_pflag);
+    dfree(d_ppart);
     dfree(d_Vx);
     dfree(d_Vh);
     dfree(d_Ut16);
@@ -262,6 +265,8 @@ approx_lstm_status ensure_batched(approx_lstm_model* m, int T, size_t Bp, int km
               "clear(hb)");
   }
   if (st == APPROX_LSTM_OK) st = grow(m->d_bc, m->bc_cap, Bp * m->H, stream, "hipMalloc(c)");
+  if (st == APPROX_LSTM_OK)
+    st = grow(m->d_ppart, m->ppart_cap, alstm::batched_ppart_floats(m->num_cu), stream, "hipMalloc(partial P)");
   return st;
 }
 
@@ -355,6 +360,7 @@ approx_lstm_status run_batched(approx_lstm_model* m, const float* x, int T, int 
   a.T = T; a.B = B; a.Bp = (int)Bp;
   a.xvec = (m->D % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1 : 0;
   a.max_wg = std::max(1, m->launch_blocks > 0 ? std::min(m->launch_blocks, m->num_cu) : m->num_cu);
+  a.Ppart = m->d_ppart; a.ppart_cap = m->ppart_cap; a.ncu = m->num_cu;
   int W = 0, slots = 0;
   if (m->batched_persistent && alstm::plan_batched_persistent(a, kmax, &W, &slots)) {
     st = ensure_persistent(m, (size_t)slots * 2 * m->G * alstm::kCohort * m->Kp,

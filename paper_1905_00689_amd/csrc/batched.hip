@@ -58,13 +58,17 @@ constexpr int kXLD = kXBK + 8;   // LDS row stride (bf16): 80 bytes, conflict-fr
 // VEC: x rows are 16-byte aligned and D is a multiple of the D padding (so
 // Dp == D): every slice of a live row is whole float4s (no bounds tests in
 // the fetch).
+// With a.xsplit > 1 workgroup blockIdx.x takes part blockIdx.x / (nM * nN)
+// of the contraction (a.Dp / a.xsplit columns) for its tile and writes the
+// partial tile to Ppart[part]; batched_xproj_sum_kernel adds the parts.
 template <bool VEC>
 __global__ void __launch_bounds__(256) batched_xproj_kernel(BatchedArgs a, int nM, int nN) {
   __shared__ __align__(16) uint16_t As[2][kXBM * kXLD];
   __shared__ __align__(16) uint16_t Bs[2][kXBN * kXLD];
   const int nt = nM * nN;
-  int tile = blockIdx.x;
-  if (nt % 8 == 0) tile = (blockIdx.x % 8) * (nt / 8) + blockIdx.x / 8;
+  const int part = blockIdx.x / nt, bid = blockIdx.x - part * nt;
+  int tile = bid;
+  if (nt % 8 == 0) tile = (bid % 8) * (nt / 8) + bid / 8;
   const int row0 = (tile % nM) * kXBM, col0 = (tile / nM) * kXBN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
@@ -93,7 +97,9 @@ __global__ void __launch_bounds__(256) batched_xproj_kernel(BatchedArgs a, int n
   }
   u32x4 ra[2][2];
   f32x4 rb[2][4];
-  const int nS = a.Dp / kXBK;
+  const int nsplit = a.xsplit > 1 ? a.xsplit : 1;
+  const int nS = a.Dp / kXBK / nsplit;   // slices of this part (even)
+  const int kbase = part * nS * kXBK;
   f32x4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -106,7 +112,7 @@ __global__ void __launch_bounds__(256) batched_xproj_kernel(BatchedArgs a, int n
   // A slice is one MFMA contraction step (32).
 #define XPROJ_FETCH(R, S)                                                                              \
   do {                                                                                                 \
-    const int k0 = (S) * kXBK;                                                                         \
+    const int k0 = kbase + (S) * kXBK;                                                                 \
     const uint16_t* va_ = a.Vx + k0;                                                                   \
     _Pragma("unroll") for (int j = 0; j < 2; ++j) ra[R][j] =                                           \
         *reinterpret_cast<const u32x4*>(va_ + aoff[j]);                                                \
@@ -177,6 +183,7 @@ __global__ void __launch_bounds__(256) batched_xproj_kernel(BatchedArgs a, int n
 #undef XPROJ_FETCH
 #undef XPROJ_STASH
   // P is column-major in tau: the 4 result rows a lane holds are adjacent
+  float* dst = nsplit > 1 ? a.Ppart + (size_t)part * NB * a.pld : a.P;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = row0 + wm * 64 + 16 * i + (lane >> 4) * 4;
@@ -185,8 +192,22 @@ __global__ void __launch_bounds__(256) batched_xproj_kernel(BatchedArgs a, int n
     for (int j = 0; j < 4; ++j) {
       const int col = col0 + wn * 64 + 16 * j + li;
       if (col < NB)
-        *reinterpret_cast<f32x4*>(a.P + (size_t)col * a.pld + row) = acc[i][j];
+        *reinterpret_cast<f32x4*>(dst + (size_t)col * a.pld + row) = acc[i][j];
     }
+  }
+}
+
+// P = Ppart[0] + Ppart[1] + ... in part order, over the [T*Bp][pld] entries
+// (pld is a multiple of 32: whole float4s).
+__global__ void __launch_bounds__(256) batched_xproj_sum_kernel(BatchedArgs a) {
+  const size_t stride = (size_t)a.T * a.Bp * a.pld;
+  const size_t n4 = stride / 4;
+  const f32x4* src = reinterpret_cast<const f32x4*>(a.Ppart);
+  f32x4* out = reinterpret_cast<f32x4*>(a.P);
+  for (size_t i = blockIdx.x * (size_t)256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) {
+    f32x4 v = src[i];
+    for (int k = 1; k < a.xsplit; ++k) v += src[k * (stride / 4) + i];
+    out[i] = v;
   }
 }
 
@@ -608,6 +629,14 @@ __global__ void __launch_bounds__(512) batched_persistent_kernel(BatchedArgs a, 
   }
 }
 
+int batched_xproj_split(int tiles, int ncu, int nslices) {
+  int s = 1;
+  while (2 * s <= 8 && (long long)tiles * 2 * s <= ncu && nslices % (4 * s) == 0) s *= 2;
+  return s;
+}
+
+size_t batched_ppart_floats(int ncu) { return (size_t)std::max(1, ncu) * kXBM * kXBN; }
+
 int plan_batched_persistent(const BatchedArgs& a, int K, int* W, int* slots) {
   const int Kl32 = ((K + 31) / 32) * 32;
   const int w = (a.H + 31) / 32;
@@ -636,11 +665,20 @@ hipError_t launch_batched(const BatchedArgs& a, const int* levels, int n_levels,
   if (kmax > 0) {
     p.rows = p.pld;
     const int nM = (p.rows + kXBM - 1) / kXBM, nN = (a.T * a.Bp + kXBN - 1) / kXBN;
+    p.xsplit = a.Ppart ? batched_xproj_split(nM * nN, a.ncu, a.Dp / kXBK) : 1;
+    if (p.xsplit > 1 && (size_t)p.xsplit * a.T * a.Bp * p.pld > a.ppart_cap) p.xsplit = 1;
+    const unsigned gx = (unsigned)(nM * nN * p.xsplit);
     if (a.xvec && a.D % kPanelDAlign == 0)
-      batched_xproj_kernel<true><<<dim3(nM * nN), dim3(256), 0, stream>>>(p, nM, nN);
+      batched_xproj_kernel<true><<<dim3(gx), dim3(256), 0, stream>>>(p, nM, nN);
     else
-      batched_xproj_kernel<false><<<dim3(nM * nN), dim3(256), 0, stream>>>(p, nM, nN);
+      batched_xproj_kernel<false><<<dim3(gx), dim3(256), 0, stream>>>(p, nM, nN);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (p.xsplit > 1) {
+      const size_t n4 = (size_t)a.T * a.Bp * p.pld / 4;
+      const unsigned gs = (unsigned)std::min<size_t>((n4 + 255) / 256, 2048);
+      batched_xproj_sum_kernel<<<dim3(gs), dim3(256), 0, stream>>>(p);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
   }
   const bool init = a.h0 != nullptr || a.c0 != nullptr;
   for (int l = 0; l < n_levels; ++l) {

@@ -250,7 +250,23 @@ struct BatchedArgs {
   unsigned tag_base; // launch sequence << 16 of level 0; level l uses tag_base + (l << 16)
   int max_wg;        // workgroups that may be resident at once (one per compute unit)
   int ztag_terms;    // z travel as tagged words when G * K (rounded up to 32) <= this
+  // x-projection with its contraction over D split in xsplit parts when it
+  // has fewer output tiles than the device has compute units: each part's
+  // tile goes to Ppart[part] ([T*Bp][pld]), then the parts are added in part
+  // order.  The split depends only on the tile count and ncu (not on the
+  // launch width), so every result keeps one summation order per shape.
+  float* Ppart;      // null: no split
+  size_t ppart_cap;  // floats of Ppart
+  int ncu;           // compute units of the device
+  int xsplit;        // set by launch_batched
 };
+
+// Largest split (a power of two, at most 8) that keeps the x-projection's
+// tiles times the split within `ncu` workgroups and gives every part an even
+// number of contraction slices (of `nslices`).
+int batched_xproj_split(int tiles, int ncu, int nslices);
+// Floats of Ppart that cover every split batched_xproj_split can choose.
+size_t batched_ppart_floats(int ncu);
 
 // Sequences per cohort of the persistent batched recurrence (the MFMA tile width).
 constexpr int kCohort = 16;
